@@ -1,0 +1,156 @@
+/*
+ * pdec — event-parallel decode attention for AMD MI355X (gfx950).
+ *
+ * One decode step of the event-factorized parallel decoding of PadCaptioner
+ * (arXiv 2607.02963, §3.4, Eq. 3): E event caption streams each issue one
+ * query token at once.  Every query attends to
+ *   (1) the shared prefix of its video: the audio-visual tokens, the
+ *       instruction and the latent global-plan tokens G^1..G^K (§3.1, §3.3),
+ *       all fully visible, and
+ *   (2) the rows of its own stream's cache: its anchor and the local tokens it
+ *       generated so far, the newest row being the current token;
+ * and never the rows of another stream (the §3.4 mask, Fig. 3).  Streams stop
+ * independently at EOS (§3.4, last paragraph); a stopped stream has no query.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Tensors are dense, row-major, in device memory, 16-byte aligned, of the
+ *    element type named by pdec_dims.dtype (float32, or bfloat16 stored as
+ *    16-bit words).  Integer arrays are int32 in device memory.
+ *  - q, out    [num_events, H_q, D]        one row per stream
+ *    lse       [num_events, H_q]  float32  natural-log log-sum-exp of the
+ *                                          scaled scores of that row
+ *    k/v_prefix [prefix rows, H_kv, D]     token-major, as a KV cache stores it
+ *    k/v_event  [num_events, event_cap, H_kv, D]  one cache per stream
+ *  - Query head h reads key/value head h / (H_q / H_kv).
+ *  - event_lens[e] = n_e, the number of visible rows of stream e's cache,
+ *    INCLUDING the current token (append first, then attend).  n_e == 0 means
+ *    the stream has ended: its out row is written as 0 and its lse as -inf.
+ *  - Scores are softmax_scale * <q, k>; softmax_scale <= 0 selects 1/sqrt(D).
+ *  - Accumulation is float32 whatever the input type; out is rounded to the
+ *    input type (round to nearest even for bfloat16).
+ *  - The caller owns every buffer.  No entry point allocates or frees device
+ *    memory; the step calls use only the caller's workspace.
+ *  - Every call is asynchronous on `stream` (a hipStream_t; NULL is the null
+ *    stream) and makes no implicit synchronisation.  Host-checkable argument
+ *    errors are reported before anything is enqueued.  Lengths held in device
+ *    memory are a caller contract (0 <= n_e <= event_cap, 0 <= prefix length
+ *    <= max_prefix_len, non-decreasing offsets); they are not checked.
+ *  - Calls sharing one workspace must not overlap in time.
+ */
+#ifndef PDEC_H
+#define PDEC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    PDEC_OK = 0,
+    PDEC_ERR_INVALID_ARG = -1, /* null / misaligned pointer, inconsistent sizes          */
+    PDEC_ERR_UNSUPPORTED = -2, /* a size or type this build has no kernel for (D, dtype) */
+    PDEC_ERR_WORKSPACE = -3,   /* workspace smaller than pdec_workspace_size()          */
+    PDEC_ERR_HIP = -4          /* a HIP runtime call or kernel launch failed             */
+} pdec_status;
+
+typedef enum { PDEC_DTYPE_F32 = 0, PDEC_DTYPE_BF16 = 1 } pdec_dtype;
+
+/* Sizes of one call.  All fields are host values. */
+typedef struct pdec_dims {
+    int32_t num_events;           /* rows of q/out/lse: E of one video, or the total over videos */
+    int32_t num_q_heads;          /* H_q, a multiple of num_kv_heads                             */
+    int32_t num_kv_heads;         /* H_kv                                                        */
+    int32_t head_dim;             /* D: 64 or 128                                                */
+    int32_t event_cap;            /* rows per stream cache, >= 1                                 */
+    int32_t max_prefix_len;       /* upper bound on any video's prefix length, >= 0              */
+    int32_t max_events_per_video; /* upper bound on streams in one video; 0 means num_events     */
+    int32_t dtype;                /* pdec_dtype of q, k, v and out                               */
+    float softmax_scale;          /* <= 0 selects 1/sqrt(head_dim)                               */
+} pdec_dims;
+
+/* Human-readable text of a pdec_status code.  Never NULL. */
+const char* pdec_strerror(int status);
+
+/*
+ * Bytes of workspace a step call with these dims needs (num_videos = 1 for
+ * pdec_attn_step).  The workspace holds the per-chunk partial softmax states
+ * (running max, normaliser and un-normalised output per query row) that the
+ * split of the prefix across compute units produces.  Returns 0 if the dims
+ * are invalid.  Pure host function: touches no device.
+ */
+size_t pdec_workspace_size(const pdec_dims* dims, int32_t num_videos);
+
+/*
+ * One parallel decode step for one video (§3.4, Eq. 3).
+ *   q           [E, H_q, D]            current query of every stream
+ *   k_prefix, v_prefix [>= L, H_kv, D] shared prefix cache of the video
+ *   k_event, v_event   [E, event_cap, H_kv, D]
+ *   event_lens  [E]  int32, device     n_e per stream (see conventions)
+ *   prefix_lens [1]  int32, device     L, 0 <= L <= dims->max_prefix_len
+ *   out         [E, H_q, D]            written for every row
+ *   lse         [E, H_q] float32, or NULL to skip it
+ *   workspace   device, >= pdec_workspace_size(dims, 1) bytes, contents ignored
+ * E = dims->num_events.  Returns a pdec_status.
+ */
+int pdec_attn_step(const pdec_dims* dims, const void* q, const void* k_prefix, const void* v_prefix,
+                   const void* k_event, const void* v_event, const int32_t* event_lens,
+                   const int32_t* prefix_lens, void* out, float* lse, void* workspace,
+                   size_t workspace_bytes, void* stream);
+
+/*
+ * One parallel decode step over a ragged batch of videos, every (video,
+ * stream) pair at once.  Video v owns prefix rows [cu_prefix[v],
+ * cu_prefix[v+1]) of the packed k/v_prefix and streams [cu_events[v],
+ * cu_events[v+1]) of q/out/lse and of the stream caches.  Streams of one video
+ * never see another video's prefix or streams.
+ *   cu_prefix, cu_events [num_videos + 1] int32, device, starting at 0;
+ *   cu_events[num_videos] == dims->num_events; every per-video prefix length
+ *   <= dims->max_prefix_len and stream count <= dims->max_events_per_video.
+ *   workspace >= pdec_workspace_size(dims, num_videos) bytes.
+ * Other arguments as for pdec_attn_step.  Returns a pdec_status.
+ */
+int pdec_attn_step_ragged(const pdec_dims* dims, int32_t num_videos, const void* q,
+                          const void* k_prefix, const void* v_prefix, const int32_t* cu_prefix,
+                          const void* k_event, const void* v_event, const int32_t* event_lens,
+                          const int32_t* cu_events, void* out, float* lse, void* workspace,
+                          size_t workspace_bytes, void* stream);
+
+/*
+ * Per-stream cache append before a step (§3.4: each live stream extends its
+ * own subchain; App. B.5: the total cache does not grow beyond what
+ * sequential decoding would hold).  For every stream e with live[e] != 0
+ * (or every stream when live is NULL): row n = event_lens[e] of its caches
+ * receives k_new[e] / v_new[e] ([H_kv, D] each) and event_lens[e] becomes
+ * n + 1.  For a stream with live[e] == 0, nothing is written and
+ * event_lens[e] becomes 0 (the stream has ended).  A live stream whose cache
+ * is full (n >= event_cap) is left unchanged.
+ *   k_new, v_new [E, H_kv, D];  k_event, v_event [E, event_cap, H_kv, D];
+ *   event_lens [E] int32, device, read and written;  live [E] int32 or NULL.
+ * E = dims->num_events.  Returns a pdec_status.
+ */
+int pdec_kv_append(const pdec_dims* dims, const void* k_new, const void* v_new, void* k_event,
+                   void* v_event, int32_t* event_lens, const int32_t* live, void* stream);
+
+/*
+ * Kernel-path selection for the shared-prefix pass, for tests and tuning:
+ * 0 = automatic (bfloat16 with >= 16 query rows per key/value head uses the
+ * matrix-core kernel, everything else the vector kernel), 1 = always the
+ * vector kernel, 2 = matrix-core kernel where the type allows it.
+ * Process-wide; returns the previous setting, or PDEC_ERR_INVALID_ARG.
+ */
+int pdec_set_path(int path);
+
+/*
+ * The kernel path (1 = vector, 2 = matrix core) and the prefix chunk length
+ * (keys per work item) a step call with these dims would use.  Host-only.
+ * Returns a pdec_status.
+ */
+int pdec_query_plan(const pdec_dims* dims, int32_t num_videos, int32_t* path, int32_t* chunk_keys);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PDEC_H */

@@ -1,0 +1,397 @@
+"""Pins of the CPU oracle to facts outside itself (no GPU).
+
+Every check here compares the oracle with something the paper or plain
+mathematics fixes: the visibility table written by hand from the §3.4 rule,
+ordinary causal decoding (Eq. 1) through torch's own attention routine,
+closed forms, invariants and brute force on tiny inputs.  Each one is chosen
+so that a plausible slip in the oracle (a dropped prefix or own row, an
+off-by-one in n_e, a leak from another stream, a wrong head group, a wrong
+sign) fails at least one of them.
+"""
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_02963_amd import workloads as wl
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _single(q, kp, vp, ke, ve, n, **kw):
+    E = q.shape[0]
+    return oracle.attn_step(q, kp, vp, ke, ve, n, [0, kp.shape[0]], [0, E], **kw)
+
+
+def _sdpa_last_row(q_last, k_seq, v_seq, scale=None):
+    """torch's causal attention (float64, CPU) over one sequence; returns the
+    output and log-sum-exp of its last position.  q_last [H_q,D];
+    k_seq/v_seq [S,H_kv,D] with H_q a multiple of H_kv."""
+    S = k_seq.shape[0]
+    H_q, D = q_last.shape
+    rng = np.random.default_rng(123)
+    q_full = rng.standard_normal((S, H_q, D))
+    q_full[-1] = q_last
+    qt = torch.from_numpy(q_full).permute(1, 0, 2)[None]
+    kt = torch.from_numpy(np.asarray(k_seq, np.float64)).permute(1, 0, 2)[None]
+    vt = torch.from_numpy(np.asarray(v_seq, np.float64)).permute(1, 0, 2)[None]
+    out = torch.nn.functional.scaled_dot_product_attention(qt, kt, vt, is_causal=True, scale=scale,
+                                                           enable_gqa=True)
+    # log-sum-exp of the last row from torch's own logsumexp over its scores
+    G = H_q // k_seq.shape[1]
+    kk = kt.repeat_interleave(G, dim=1)
+    sc = (qt[0, :, -1:, :] @ kk[0].transpose(-1, -2))[:, 0, :] * (scale if scale else 1 / math.sqrt(D))
+    lse = torch.logsumexp(sc, dim=-1)
+    return out[0, :, -1, :].numpy(), lse.numpy()
+
+
+def _f64(x):
+    return wl.bf16_widen(x).astype(np.float64) if x.dtype == np.uint16 else np.asarray(x, np.float64)
+
+
+# ---------------------------------------------------------------------------
+# The mask itself, against the hand-written table
+# ---------------------------------------------------------------------------
+
+def _golden_masks():
+    cases, cur = [], None
+    with open(os.path.join(GOLDEN, "mask_fig3.txt")) as f:
+        for line in f:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            if line.startswith("case"):
+                kv = dict(tok.split("=") for tok in line.split()[1:])
+                cur = dict(L=int(kv["L"]), E=int(kv["E"]), cap=int(kv["cap"]),
+                           n=[int(x) for x in kv["n"].split(",")], rows=[])
+                cases.append(cur)
+            else:
+                cur["rows"].append([int(x) for x in line.split()])
+    return cases
+
+
+@pytest.mark.parametrize("case", _golden_masks(), ids=lambda c: f"L{c['L']}E{c['E']}n{c['n']}")
+def test_mask_matches_hand_written_table(case):
+    got = oracle.build_mask(case["L"], case["E"], case["cap"], case["n"])
+    want = np.array(case["rows"], dtype=bool)
+    assert got.shape == want.shape
+    assert np.array_equal(got, want)
+
+
+# ---------------------------------------------------------------------------
+# (a) one stream is ordinary causal decoding (Eq. 1)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("L,n,H_q,H_kv,D", [(37, 5, 4, 1, 64), (100, 1, 6, 2, 16), (0, 9, 3, 3, 8),
+                                             (64, 64, 28, 4, 128)])
+def test_single_stream_is_causal_decode(L, n, H_q, H_kv, D):
+    s = wl.make_step(dtype="f32", H_q=H_q, H_kv=H_kv, D=D, prefix_lens=(L,), events_per_video=(1,),
+                     event_lens=[n], cap=n + 3, sigma=1.0, seed=L + n)
+    out, lse = _single(s.q, s.k_prefix, s.v_prefix, s.k_event, s.v_event, s.event_lens)
+    seq_k = np.concatenate([s.k_prefix, s.k_event[0, :n]])
+    seq_v = np.concatenate([s.v_prefix, s.v_event[0, :n]])
+    ro, rl = _sdpa_last_row(_f64(s.q[0]), _f64(seq_k), _f64(seq_v))
+    np.testing.assert_allclose(out[0], ro, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(lse[0], rl, rtol=0, atol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# (b) each stream equals decoding prefix + its own rows alone
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_each_stream_equals_its_own_sequence(dtype):
+    s = wl.make_step(dtype=dtype, H_q=8, H_kv=2, D=32, prefix_lens=(50,), events_per_video=(5,),
+                     event_lens=[1, 4, 7, 2, 5], cap=8, sigma=1.0, seed=7)
+    out, lse = _single(s.q, s.k_prefix, s.v_prefix, s.k_event, s.v_event, s.event_lens)
+    for e in range(5):
+        n = s.event_lens[e]
+        seq_k = np.concatenate([s.k_prefix, s.k_event[e, :n]])
+        seq_v = np.concatenate([s.v_prefix, s.v_event[e, :n]])
+        ro, rl = _sdpa_last_row(_f64(s.q[e]), _f64(seq_k), _f64(seq_v))
+        np.testing.assert_allclose(out[e], ro, rtol=0, atol=1e-12)
+        np.testing.assert_allclose(lse[e], rl, rtol=0, atol=1e-12)
+
+
+def test_planted_own_rows_dominate_and_other_streams_never_leak():
+    """Each stream's own rows carry a key aligned with its query, so they take
+    almost all the weight; a leak of another stream's rows, or a missing own
+    row, moves the output by O(1)."""
+    s = wl.make_step(dtype="f32", H_q=2, H_kv=1, D=16, prefix_lens=(40,), events_per_video=(3,),
+                     event_lens=[2, 3, 1], cap=4, sigma=0.1, seed=3)
+    for e in range(3):
+        for t in range(s.cap):
+            # score of an own row = 40 for both heads' queries (heads share the kv head)
+            s.q[e, 1] = s.q[e, 0]
+            s.k_event[e, t, 0] = 40.0 * 4.0 * s.q[e, 0] / np.dot(s.q[e, 0], s.q[e, 0])
+            s.v_event[e, t, 0] = 10.0 * (e + 1) + t
+    out, _ = _single(s.q, s.k_prefix, s.v_prefix, s.k_event, s.v_event, s.event_lens)
+    for e in range(3):
+        n = s.event_lens[e]
+        expect = np.mean([10.0 * (e + 1) + t for t in range(n)])
+        np.testing.assert_allclose(out[e], np.full((2, 16), expect), atol=1e-9)
+
+
+# ---------------------------------------------------------------------------
+# (c) softmax rows sum to one; masked weights are exactly zero
+# ---------------------------------------------------------------------------
+
+def test_weights_sum_to_one_and_masked_are_zero():
+    s = wl.make_step(dtype="bf16", H_q=4, H_kv=2, D=32, prefix_lens=(33,), events_per_video=(4,),
+                     event_lens=[3, 0, 6, 1], cap=6, seed=11)
+    out, lse, probs = _single(s.q, s.k_prefix, s.v_prefix, s.k_event, s.v_event, s.event_lens,
+                              want_probs=True)
+    mask = oracle.build_mask(33, 4, 6, s.event_lens)
+    for e in range(4):
+        for h in range(4):
+            p = probs[e, h]
+            assert np.all(p[~mask[e]] == 0.0)
+            if s.event_lens[e] == 0:
+                assert np.all(p == 0.0)
+            else:
+                assert abs(p.sum() - 1.0) < 1e-12
+                assert np.all(p[mask[e]] > 0)
+
+
+# ---------------------------------------------------------------------------
+# (d) permuting streams permutes the outputs exactly
+# ---------------------------------------------------------------------------
+
+def test_stream_permutation_invariance():
+    s = wl.make_step(dtype="bf16", H_q=8, H_kv=2, D=64, prefix_lens=(70,), events_per_video=(6,),
+                     own_len_range=(0, 9), cap=10, seed=5)
+    out, lse = _single(s.q, s.k_prefix, s.v_prefix, s.k_event, s.v_event, s.event_lens)
+    perm = np.array([3, 0, 5, 1, 4, 2])
+    out_p, lse_p = _single(s.q[perm], s.k_prefix, s.v_prefix, s.k_event[perm], s.v_event[perm],
+                           s.event_lens[perm])
+    assert np.array_equal(out_p, out[perm])
+    assert np.array_equal(lse_p, lse[perm])
+
+
+# ---------------------------------------------------------------------------
+# Closed forms
+# ---------------------------------------------------------------------------
+
+def test_zero_keys_give_uniform_weights():
+    """k = 0: every visible key scores 0, so out is the mean of the visible
+    values and lse = ln(L + n_e)."""
+    s = wl.make_step(dtype="f32", H_q=3, H_kv=1, D=8, prefix_lens=(21,), events_per_video=(4,),
+                     event_lens=[1, 5, 0, 3], cap=5, sigma=1.0, seed=2)
+    s.k_prefix[:] = 0
+    s.k_event[:] = 0
+    out, lse = _single(s.q, s.k_prefix, s.v_prefix, s.k_event, s.v_event, s.event_lens)
+    for e in range(4):
+        n = s.event_lens[e]
+        if n == 0:
+            assert np.all(out[e] == 0) and np.all(np.isneginf(lse[e]))
+            continue
+        vis = np.concatenate([s.v_prefix[:, 0], s.v_event[e, :n, 0]]).astype(np.float64)
+        for h in range(3):
+            np.testing.assert_allclose(out[e, h], vis.mean(axis=0), atol=1e-12)
+            assert abs(lse[e, h] - math.log(21 + n)) < 1e-12
+
+
+def test_constant_values_pass_through():
+    s = wl.make_step(dtype="f32", H_q=4, H_kv=2, D=16, prefix_lens=(17,), events_per_video=(3,),
+                     event_lens=[2, 1, 4], cap=4, sigma=1.0, seed=9)
+    c = np.linspace(-2, 3, 16, dtype=np.float32)
+    s.v_prefix[:] = c
+    s.v_event[:] = c
+    out, _ = _single(s.q, s.k_prefix, s.v_prefix, s.k_event, s.v_event, s.event_lens)
+    np.testing.assert_allclose(out, np.broadcast_to(c, out.shape), atol=1e-12)
+
+
+def test_worked_example_by_hand():
+    """D=1, scale 1, q=1.  Prefix keys 0 and 1, own keys 2 (one other stream
+    holds key 50, which must stay invisible).  Weights are e^0:e^1:e^2 with
+    values 6, 0, 2:  out = (6 + 2e^2) / (1 + e + e^2), lse = ln(1 + e + e^2)."""
+    q = np.array([[[1.0]], [[1.0]]], np.float32)
+    kp = np.array([[[0.0]], [[1.0]]], np.float32)
+    vp = np.array([[[6.0]], [[0.0]]], np.float32)
+    ke = np.array([[[[2.0]]], [[[50.0]]]], np.float32)
+    ve = np.array([[[[2.0]]], [[[-9.0]]]], np.float32)
+    out, lse = _single(q, kp, vp, ke, ve, [1, 1], scale=1.0)
+    e = math.e
+    assert abs(out[0, 0, 0] - (6 + 2 * e * e) / (1 + e + e * e)) < 1e-14
+    assert abs(lse[0, 0] - math.log(1 + e + e * e)) < 1e-14
+    # the second stream sees the prefix and its own key 50
+    w = np.exp(np.array([0.0, 1.0, 50.0]) - 50.0)
+    assert abs(out[1, 0, 0] - (w @ np.array([6.0, 0.0, -9.0])) / w.sum()) < 1e-12
+    assert abs(lse[1, 0] - (50.0 + math.log(w.sum()))) < 1e-12
+
+
+def test_planted_prefix_peak():
+    """One prefix key aligned with every query far above the rest: out is that
+    key's value row, lse is its score (up to exp(-gap))."""
+    s = wl.make_step(dtype="f32", H_q=2, H_kv=1, D=32, prefix_lens=(64,), events_per_video=(2,),
+                     event_lens=[3, 2], cap=3, sigma=0.05, seed=4)
+    u = np.ones(32, np.float32) / math.sqrt(32)
+    s.q[:, :, :] = u
+    s.k_prefix[17, 0] = 400.0 * u
+    out, lse = _single(s.q, s.k_prefix, s.v_prefix, s.k_event, s.v_event, s.event_lens)
+    top = float(np.dot(s.q[0, 0].astype(np.float64), s.k_prefix[17, 0].astype(np.float64))) / math.sqrt(32)
+    for e in range(2):
+        for h in range(2):
+            np.testing.assert_allclose(out[e, h], s.v_prefix[17, 0], atol=1e-9)
+            assert abs(lse[e, h] - top) < 1e-9
+
+
+def test_dead_stream_outputs():
+    s = wl.make_step(dtype="bf16", H_q=4, H_kv=1, D=8, prefix_lens=(9,), events_per_video=(3,),
+                     event_lens=[0, 2, 0], cap=2, seed=1)
+    out, lse = _single(s.q, s.k_prefix, s.v_prefix, s.k_event, s.v_event, s.event_lens)
+    assert np.all(out[[0, 2]] == 0) and np.all(np.isneginf(lse[[0, 2]]))
+    assert np.all(np.isfinite(out[1])) and np.all(np.isfinite(lse[1]))
+
+
+# ---------------------------------------------------------------------------
+# Head grouping, batching, precision, scale
+# ---------------------------------------------------------------------------
+
+def test_query_head_group_reads_its_kv_head():
+    """H_q=6, H_kv=3: query heads 2h, 2h+1 read key/value head h (contiguous
+    groups).  Their rows must equal a one-kv-head problem on that head alone."""
+    s = wl.make_step(dtype="f32", H_q=6, H_kv=3, D=16, prefix_lens=(30,), events_per_video=(2,),
+                     event_lens=[2, 4], cap=4, sigma=1.0, seed=21)
+    out, lse = _single(s.q, s.k_prefix, s.v_prefix, s.k_event, s.v_event, s.event_lens)
+    for g in range(3):
+        sub = _single(np.ascontiguousarray(s.q[:, 2 * g:2 * g + 2]), np.ascontiguousarray(s.k_prefix[:, g:g + 1]),
+                      np.ascontiguousarray(s.v_prefix[:, g:g + 1]), np.ascontiguousarray(s.k_event[:, :, g:g + 1]),
+                      np.ascontiguousarray(s.v_event[:, :, g:g + 1]), s.event_lens)
+        assert np.array_equal(out[:, 2 * g:2 * g + 2], sub[0])
+        assert np.array_equal(lse[:, 2 * g:2 * g + 2], sub[1])
+
+
+def test_ragged_batch_is_videos_side_by_side():
+    s = wl.make_step(dtype="bf16", H_q=4, H_kv=2, D=32, prefix_lens=(20, 0, 45), events_per_video=(2, 3, 1),
+                     own_len_range=(0, 5), cap=6, seed=8)
+    out, lse = oracle.attn_step(s.q, s.k_prefix, s.v_prefix, s.k_event, s.v_event, s.event_lens,
+                                s.cu_prefix, s.cu_events)
+    for v in range(3):
+        p0, p1 = s.cu_prefix[v], s.cu_prefix[v + 1]
+        e0, e1 = s.cu_events[v], s.cu_events[v + 1]
+        o, l = _single(s.q[e0:e1], s.k_prefix[p0:p1], s.v_prefix[p0:p1], s.k_event[e0:e1],
+                       s.v_event[e0:e1], s.event_lens[e0:e1])
+        assert np.array_equal(out[e0:e1], o) and np.array_equal(lse[e0:e1], l)
+
+
+def test_bf16_inputs_are_widened_exactly():
+    s = wl.make_step(dtype="bf16", H_q=4, H_kv=1, D=32, prefix_lens=(19,), events_per_video=(2,),
+                     event_lens=[3, 1], cap=3, seed=6)
+    out, lse = _single(s.q, s.k_prefix, s.v_prefix, s.k_event, s.v_event, s.event_lens)
+    w = wl.bf16_widen
+    out2, lse2 = _single(w(s.q), w(s.k_prefix), w(s.v_prefix), w(s.k_event), w(s.v_event), s.event_lens)
+    assert np.array_equal(out, out2) and np.array_equal(lse, lse2)
+
+
+def test_explicit_scale_matches_default():
+    s = wl.make_step(dtype="f32", H_q=2, H_kv=1, D=64, prefix_lens=(10,), events_per_video=(2,),
+                     event_lens=[1, 2], cap=2, sigma=1.0, seed=12)
+    a = _single(s.q, s.k_prefix, s.v_prefix, s.k_event, s.v_event, s.event_lens)
+    b = _single(s.q, s.k_prefix, s.v_prefix, s.k_event, s.v_event, s.event_lens, scale=1 / 8)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+
+
+def test_row_select_computes_only_selected_rows_identically():
+    s = wl.make_step(dtype="bf16", H_q=4, H_kv=2, D=32, prefix_lens=(25,), events_per_video=(3,),
+                     own_len_range=(0, 4), cap=5, seed=13)
+    full = _single(s.q, s.k_prefix, s.v_prefix, s.k_event, s.v_event, s.event_lens)
+    sel = np.zeros((3, 4), bool)
+    sel[1, 2] = sel[2, 0] = True
+    part = _single(s.q, s.k_prefix, s.v_prefix, s.k_event, s.v_event, s.event_lens, row_select=sel)
+    assert np.array_equal(part[0][sel], full[0][sel]) and np.array_equal(part[1][sel], full[1][sel])
+    assert np.all(np.isnan(part[1][~sel]))
+
+
+def test_float32_variant_drift_is_small():
+    s = wl.tiny_f32()
+    a = oracle.attn_step(s.q, s.k_prefix, s.v_prefix, s.k_event, s.v_event, s.event_lens, s.cu_prefix,
+                         s.cu_events)
+    b = oracle.attn_step(s.q, s.k_prefix, s.v_prefix, s.k_event, s.v_event, s.event_lens, s.cu_prefix,
+                         s.cu_events, precision="f32")
+    assert np.max(np.abs(a[0] - b[0])) < 2e-6
+    assert np.max(np.abs(a[1] - b[1])) < 2e-6
+
+
+def test_thread_count_does_not_change_results():
+    s = wl.make_step(dtype="bf16", H_q=8, H_kv=2, D=64, prefix_lens=(300,), events_per_video=(5,),
+                     own_len_range=(0, 20), cap=21, seed=14)
+    a = _single(s.q, s.k_prefix, s.v_prefix, s.k_event, s.v_event, s.event_lens, threads=1)
+    b = _single(s.q, s.k_prefix, s.v_prefix, s.k_event, s.v_event, s.event_lens, threads=4)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+
+
+# ---------------------------------------------------------------------------
+# Tiny brute force: every length combination
+# ---------------------------------------------------------------------------
+
+def test_brute_force_all_lengths_tiny():
+    """E=3 streams, cap 2, L in {0,1,3}: every n in {0,1,2}^3 against a
+    direct evaluation over the list [prefix rows, own rows] written with
+    Python loops."""
+    rng = np.random.default_rng(0)
+    H_q, H_kv, D, cap, E = 2, 1, 2, 2, 3
+    for L in (0, 1, 3):
+        q = rng.standard_normal((E, H_q, D)).astype(np.float32)
+        kp = rng.standard_normal((L, H_kv, D)).astype(np.float32)
+        vp = rng.standard_normal((L, H_kv, D)).astype(np.float32)
+        ke = rng.standard_normal((E, cap, H_kv, D)).astype(np.float32)
+        ve = rng.standard_normal((E, cap, H_kv, D)).astype(np.float32)
+        for n in np.ndindex(3, 3, 3):
+            n = np.array(n, np.int32)
+            out, lse = _single(q, kp, vp, ke, ve, n)
+            for e in range(E):
+                for h in range(H_q):
+                    if n[e] == 0:
+                        assert np.all(out[e, h] == 0) and np.isneginf(lse[e, h])
+                        continue
+                    keys = [kp[j, 0] for j in range(L)] + [ke[e, t, 0] for t in range(n[e])]
+                    vals = [vp[j, 0] for j in range(L)] + [ve[e, t, 0] for t in range(n[e])]
+                    sc = [sum(float(q[e, h, d]) * float(k[d]) for d in range(D)) / math.sqrt(D) for k in keys]
+                    mx = max(sc)
+                    w = [math.exp(x - mx) for x in sc]
+                    tot = sum(w)
+                    for d in range(D):
+                        ref = sum(wi * float(v[d]) for wi, v in zip(w, vals)) / tot
+                        assert abs(out[e, h, d] - ref) < 1e-12
+                    assert abs(lse[e, h] - (mx + math.log(tot))) < 1e-12
+
+
+# ---------------------------------------------------------------------------
+# Decode loop: appends, independent EOS, and the single-chain comparator
+# ---------------------------------------------------------------------------
+
+def test_decode_loop_matches_step_with_hand_built_caches():
+    lp = wl.make_loop(dtype="bf16", H_q=4, H_kv=2, D=32, L=40, E=3, steps=7, eos_range=(2, 7), seed=3)
+    out, lse = oracle.decode_loop(lp.k_prefix, lp.v_prefix, lp.q_steps, lp.k_new, lp.v_new, lp.eos_step,
+                                  cap=lp.cap)
+    E = lp.num_events
+    for s in range(lp.steps):
+        n = np.array([s + 1 if s < lp.eos_step[e] else 0 for e in range(E)], np.int32)
+        ke = np.zeros((E, lp.cap, 2, 32), np.uint16)
+        ve = np.zeros_like(ke)
+        for e in range(E):
+            if n[e]:
+                ke[e, :n[e]] = lp.k_new[:n[e], e]
+                ve[e, :n[e]] = lp.v_new[:n[e], e]
+        o, l = _single(lp.q_steps[s], lp.k_prefix, lp.v_prefix, ke, ve, n)
+        assert np.array_equal(out[s], o) and np.array_equal(lse[s], l)
+        for e in range(E):
+            if s >= lp.eos_step[e]:
+                assert np.all(out[s, e] == 0) and np.all(np.isneginf(lse[s, e]))
+
+
+def test_sequential_comparator_is_causal_decode():
+    lp = wl.make_loop(dtype="f32", H_q=2, H_kv=1, D=16, L=12, E=2, steps=4, eos_range=(2, 4), seed=5)
+    sq = lp.sequential()
+    out, lse = oracle.decode_loop(sq.k_prefix, sq.v_prefix, sq.q_steps, sq.k_new, sq.v_new, sq.eos_step,
+                                  cap=sq.cap)
+    for s in range(sq.steps):
+        seq_k = np.concatenate([sq.k_prefix, sq.k_new[:s + 1, 0]])
+        seq_v = np.concatenate([sq.v_prefix, sq.v_new[:s + 1, 0]])
+        ro, rl = _sdpa_last_row(_f64(sq.q_steps[s, 0]), _f64(seq_k), _f64(seq_v))
+        np.testing.assert_allclose(out[s, 0], ro, atol=1e-12)
+        np.testing.assert_allclose(lse[s, 0], rl, atol=1e-12)
