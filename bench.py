@@ -1,0 +1,191 @@
+"""Benchmark of the event-parallel decode attention step on one MI355X.
+
+One "step" is one full decode step of the attention layer: the split pass
+over the shared prefix and every stream's own rows, and the merge, for every
+(stream, head) row of the workload.  Default workload: prefix 32768 tokens,
+32 event streams, H_q=28, H_kv=4, D=128, bf16 (the headline shape).
+
+Protocol
+  * inputs are resident in HBM before timing; several copies of the step's
+    inputs (distinct allocations, >= 512 MB together) are cycled so the
+    256 MB last-level cache cannot serve the prefix from one step to the next;
+  * W untimed warm-up steps, then K timed steps back to back between two HIP
+    events on the launch stream (synchronised on both sides);
+  * a second pass of K steps brackets only the split kernel with HIP events
+    (library measurement hook; same work) to give that kernel's average
+    duration, from which its achieved HBM bandwidth is computed on its
+    algorithmic bytes;
+  * the CPU oracle runs the same step on the host cores (one full step).
+
+Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "µs/decode step + achieved HBM GB/s (% of peak) at prefix 32k, E=32 events"
+HBM_PEAK_GBPS = 8000.0
+ROTATE_BYTES = 512 << 20
+
+
+def _log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def _dev_step(s, torch):
+    def f(a):
+        if s.dtype == "bf16":
+            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+        return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+    def i(a):
+        return torch.from_numpy(np.ascontiguousarray(np.asarray(a, np.int32))).cuda()
+
+    return dict(q=f(s.q), k_prefix=f(s.k_prefix), v_prefix=f(s.v_prefix), k_event=f(s.k_event),
+                v_event=f(s.v_event), event_lens=i(s.event_lens), cu_prefix=i(s.cu_prefix),
+                cu_events=i(s.cu_events), prefix_lens=i(s.prefix_lens[:1]))
+
+
+def _clone_set(d):
+    return {k: v.clone() for k, v in d.items()}
+
+
+def split_kernel_bytes(s) -> int:
+    """Algorithmic bytes of the split pass: prefix K/V once per kv head, every
+    stream's visible own K/V rows, and q."""
+    b = s.elem_bytes
+    row = s.H_kv * s.D * b
+    return 2 * int(s.cu_prefix[-1]) * row + 2 * int(s.event_lens.sum()) * row + s.num_events * s.H_q * s.D * b
+
+
+def cpu_baseline(s):
+    """The oracle (as it stands) on the host cores: one full step, all rows."""
+    sys.path.insert(0, os.path.join(ROOT, "oracle"))
+    import oracle
+    threads = oracle.max_threads()
+    t0 = time.perf_counter()
+    oracle.attn_step(s.q, s.k_prefix, s.v_prefix, s.k_event, s.v_event, s.event_lens, s.cu_prefix, s.cu_events,
+                     scale=s.scale, threads=threads)
+    dt = time.perf_counter() - t0
+    return {"value": round(dt * 1e6, 1), "unit": "us/step", "cores": threads, "kind": "oracle",
+            "sample": f"one full step of {s.name}: all {s.num_events * s.H_q} (stream, head) rows, float64 "
+                      f"dense-mask oracle, OpenMP over rows"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="long_32k", help="long_32k | single_8k | ragged_16 | tiny_f32")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+                          "n_gpus_requested": args.gpus}))
+        sys.exit(2)
+
+    import torch
+
+    from paper_2607_02963_amd import pdec
+    from paper_2607_02963_amd import workloads as wl
+
+    torch.cuda.set_device(0)
+    s = wl.STEP_WORKLOADS[args.workload]()
+    ragged = s.num_videos > 1
+    base = _dev_step(s, torch)
+    set_bytes = sum(t.numel() * t.element_size() for t in base.values())
+    nsets = max(1, math.ceil(ROTATE_BYTES / set_bytes))
+    sets = [base] + [_clone_set(base) for _ in range(nsets - 1)]
+    out = torch.empty_like(base["q"])
+    lse = torch.empty(s.num_events, s.H_q, dtype=torch.float32, device="cuda")
+    max_ev = int(s.events_per_video.max())
+    max_L = int(s.prefix_lens.max())
+    dims = pdec.make_dims(s.num_events, s.H_q, s.H_kv, s.D, s.cap, max_L, pdec._dtype_code(out), s.scale, max_ev)
+    ws = torch.empty(pdec.workspace_size(dims, s.num_videos), dtype=torch.uint8, device="cuda")
+    path, chunk = pdec.query_plan(dims, s.num_videos)
+    stream = torch.cuda.current_stream()
+
+    def step(i):
+        d = sets[i % nsets]
+        if ragged:
+            pdec.attn_step_ragged(d["q"], d["k_prefix"], d["v_prefix"], d["cu_prefix"], d["k_event"], d["v_event"],
+                                  d["event_lens"], d["cu_events"], max_prefix_len=max_L, max_events_per_video=max_ev,
+                                  out=out, lse=lse, workspace=ws, scale=s.scale, stream=stream)
+        else:
+            pdec.attn_step(d["q"], d["k_prefix"], d["v_prefix"], d["k_event"], d["v_event"], d["event_lens"],
+                           d["prefix_lens"], out=out, lse=lse, workspace=ws, scale=s.scale, stream=stream)
+
+    _log(f"bench: workload {s.name} path={path} chunk={chunk} sets={nsets} x {set_bytes / 1e6:.1f} MB")
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for i in range(args.steps):
+        step(i)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / args.steps
+    _log(f"bench: timed {args.steps} steps: {ms * 1e3:.2f} us/step")
+
+    timer = pdec.SplitTimer(args.steps)
+    with timer:
+        for i in range(args.steps):
+            step(i)
+    torch.cuda.synchronize()
+    kms = timer.durations_ms(args.steps)
+    timer.close()
+    split_ms = float(np.mean(kms))
+    _log(f"bench: split kernel {split_ms * 1e3:.2f} us avg (min {min(kms) * 1e3:.2f}, max {max(kms) * 1e3:.2f})")
+
+    alg = s.algorithmic_bytes()
+    gbps = alg / (ms * 1e-3) / 1e9
+    kbytes = split_kernel_bytes(s)
+    kgbps = kbytes / (split_ms * 1e-3) / 1e9
+    live = int((s.event_lens > 0).sum())
+    rec = {
+        "metric": METRIC,
+        "value": round(ms * 1e3, 3),
+        "unit": "us/step",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 6),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": s.dtype,
+        "data": "synthetic",
+        "config": {"workload": s.name, "videos": s.num_videos, "prefix_len": max_L if not ragged else int(s.cu_prefix[-1]),
+                   "events": s.num_events, "H_q": s.H_q, "H_kv": s.H_kv, "head_dim": s.D, "seed": s.seed,
+                   "kernel_path": {1: "valu", 2: "mfma"}[path], "chunk_keys": chunk},
+        "achieved_GBps": round(gbps, 1),
+        "hbm_peak_frac": round(gbps / HBM_PEAK_GBPS, 4),
+        "algorithmic_bytes_per_step": alg,
+        "tokens_per_s": round(live / (ms * 1e-3), 1),
+        "roofline": {"bound": "hbm", "achieved": round(kgbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(kgbps / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "kernel": "split pass (shared prefix + stream rows)", "kernel_us": round(split_ms * 1e3, 3),
+                     "kernel_algorithmic_bytes": kbytes},
+    }
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = cpu_baseline(s)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

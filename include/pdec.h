@@ -16,7 +16,8 @@
  * ---------------------------------------
  *  - Tensors are dense, row-major, in device memory, 16-byte aligned, of the
  *    element type named by pdec_dims.dtype (float32, or bfloat16 stored as
- *    16-bit words).  Integer arrays are int32 in device memory.
+ *    16-bit words).  Integer arrays (lengths, offsets, flags) are int32 in
+ *    device memory, 4-byte aligned; so is lse.
  *  - q, out    [num_events, H_q, D]        one row per stream
  *    lse       [num_events, H_q]  float32  natural-log log-sum-exp of the
  *                                          scaled scores of that row
@@ -87,6 +88,7 @@ size_t pdec_workspace_size(const pdec_dims* dims, int32_t num_videos);
  * One parallel decode step for one video (§3.4, Eq. 3).
  *   q           [E, H_q, D]            current query of every stream
  *   k_prefix, v_prefix [>= L, H_kv, D] shared prefix cache of the video
+ *                      (may be NULL when dims->max_prefix_len == 0)
  *   k_event, v_event   [E, event_cap, H_kv, D]
  *   event_lens  [E]  int32, device     n_e per stream (see conventions)
  *   prefix_lens [1]  int32, device     L, 0 <= L <= dims->max_prefix_len
@@ -149,6 +151,17 @@ int pdec_set_path(int path);
  * Returns a pdec_status.
  */
 int pdec_query_plan(const pdec_dims* dims, int32_t num_videos, int32_t* path, int32_t* chunk_keys);
+
+/*
+ * Measurement hook.  With n > 0, the i-th step call made after this call
+ * brackets its split pass (the kernel that reads the shared prefix and the
+ * stream caches) with hipEventRecord(start_events[i % n]) and
+ * hipEventRecord(stop_events[i % n]) on the call's stream, so a caller can
+ * time that kernel alone without changing the work done.  The events are
+ * hipEvent_t handles owned by the caller.  n = 0 (or NULL arrays) turns the
+ * hook off.  Process-wide, not thread-safe.  Returns a pdec_status.
+ */
+int pdec_set_split_timer(void* const* start_events, void* const* stop_events, int n);
 
 #ifdef __cplusplus
 }

@@ -1,0 +1,328 @@
+// Host side of libpdec: argument validation, work planning and kernel
+// dispatch for the C ABI declared in include/pdec.h.
+//
+// A step is two launches on the caller's stream:
+//   1. the split pass — prefix items (video, kv head, chunk, row group) and
+//      tail items (stream, kv head, row group), each writing one partial
+//      softmax state per query row into the workspace;
+//   2. the merge — one wave per (stream, head) row, writing out and lse.
+// Nothing is allocated per call; the workspace is the caller's.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <atomic>
+#include <cmath>
+#include <cstdint>
+#include <cstdlib>
+
+#include "pdec.h"
+
+#include "kernel_append.h"
+#include "kernel_merge.h"
+#include "kernel_mfma.h"
+#include "kernel_valu.h"
+
+namespace {
+
+using namespace pdec;
+
+constexpr int kPathValu = 1;
+constexpr int kPathMfma = 2;
+constexpr int kTargetItems = 256;   // MI355X compute units: one item per CU per wave of items
+constexpr int kMfmaMaxTiles = 4;    // 16-row tiles per matrix-core item
+constexpr int kKeyAlign = 128;      // chunk lengths are whole 128-key blocks
+
+std::atomic<int> g_path_override{0};
+
+// measurement hook (pdec_set_split_timer)
+void* const* g_timer_start = nullptr;
+void* const* g_timer_stop = nullptr;
+int g_timer_n = 0;
+long g_timer_calls = 0;
+
+struct Plan {
+    int path;
+    int rows_per_item;
+    int nt;            // row tiles per item (matrix-core path)
+    int rg_max;
+    int tail_rg;
+    int chunk;
+    int max_chunks;
+    int slots;
+    long n_prefix_items;
+    long n_tail_items;
+    size_t ws_bytes;
+};
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+
+int validate_dims(const pdec_dims* d, int num_videos)
+{
+    if (!d) return PDEC_ERR_INVALID_ARG;
+    if (num_videos < 1 || d->num_events < 1 || d->num_q_heads < 1 || d->num_kv_heads < 1 ||
+        d->num_q_heads % d->num_kv_heads != 0 || d->event_cap < 1 || d->max_prefix_len < 0 ||
+        d->max_events_per_video < 0 || d->max_events_per_video > d->num_events)
+        return PDEC_ERR_INVALID_ARG;
+    if (d->dtype != PDEC_DTYPE_F32 && d->dtype != PDEC_DTYPE_BF16) return PDEC_ERR_UNSUPPORTED;
+    if (d->head_dim != 64 && d->head_dim != 128) return PDEC_ERR_UNSUPPORTED;
+    if (!(d->softmax_scale <= 0.f) && !std::isfinite(d->softmax_scale)) return PDEC_ERR_INVALID_ARG;
+    // index arithmetic inside the kernels is 32-bit for row counts
+    const long rows = (long)d->num_events * d->num_q_heads;
+    if (rows > (1L << 30)) return PDEC_ERR_UNSUPPORTED;
+    return PDEC_OK;
+}
+
+int ceil_div(long a, long b) { return (int)((a + b - 1) / b); }
+
+Plan make_plan(const pdec_dims* d, int num_videos)
+{
+    Plan p{};
+    const int G = d->num_q_heads / d->num_kv_heads;
+    const int ev = d->max_events_per_video > 0 ? d->max_events_per_video : d->num_events;
+    const long rows_max = (long)ev * G;  // query rows per (video, kv head)
+    int path = (d->dtype == PDEC_DTYPE_BF16 && rows_max >= 16) ? kPathMfma : kPathValu;
+    const int ov = g_path_override.load();
+    if (ov == kPathValu) path = kPathValu;
+    if (ov == kPathMfma && d->dtype == PDEC_DTYPE_BF16) path = kPathMfma;
+    p.path = path;
+    if (path == kPathMfma) {
+        const int tiles = ceil_div(rows_max, 16);
+        const int groups = ceil_div(tiles, kMfmaMaxTiles);
+        p.nt = ceil_div(tiles, groups);
+        p.rows_per_item = 16 * p.nt;
+    } else {
+        p.nt = 0;
+        p.rows_per_item = rows_max <= 8 ? 8 : 16;
+    }
+    p.rg_max = ceil_div(rows_max, p.rows_per_item);
+    p.tail_rg = ceil_div(G, p.rows_per_item);
+    // chunk length: spread the prefix of the batch over about kTargetItems items
+    const long work = (long)std::max(d->max_prefix_len, 1) * num_videos * d->num_kv_heads * p.rg_max;
+    long chunk = (work + kTargetItems - 1) / kTargetItems;
+    chunk = (chunk + kKeyAlign - 1) / kKeyAlign * kKeyAlign;
+    chunk = std::max<long>(chunk, kKeyAlign);
+    p.chunk = (int)std::min<long>(chunk, 1L << 30);
+    p.max_chunks = std::max(1, ceil_div(d->max_prefix_len, p.chunk));
+    p.slots = p.max_chunks + 1;
+    p.n_prefix_items = (long)num_videos * d->num_kv_heads * p.max_chunks * p.rg_max;
+    p.n_tail_items = (long)d->num_events * d->num_kv_heads * p.tail_rg;
+    const size_t rows = (size_t)d->num_events * d->num_q_heads;
+    p.ws_bytes = (size_t)p.slots * rows * ((size_t)d->head_dim + 2) * sizeof(float);
+    return p;
+}
+
+int launch_status()
+{
+    const hipError_t e = hipGetLastError();
+    return e == hipSuccess ? PDEC_OK : PDEC_ERR_HIP;
+}
+
+template <int D, int NT>
+void launch_mfma_nt(const StepArgs& a, int grid, hipStream_t s)
+{
+    hipLaunchKernelGGL((split_mfma_kernel<D, NT>), dim3(grid), dim3(256), 0, s, a);
+}
+
+template <int D>
+void launch_mfma(const StepArgs& a, int nt, int grid, hipStream_t s)
+{
+    switch (nt) {
+    case 1: launch_mfma_nt<D, 1>(a, grid, s); break;
+    case 2: launch_mfma_nt<D, 2>(a, grid, s); break;
+    case 3: launch_mfma_nt<D, 3>(a, grid, s); break;
+    default: launch_mfma_nt<D, 4>(a, grid, s); break;
+    }
+}
+
+template <typename T, int D>
+void launch_valu(const StepArgs& a, int rt, int grid, hipStream_t s)
+{
+    if (rt == 8) hipLaunchKernelGGL((split_valu_kernel<T, D, 8>), dim3(grid), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((split_valu_kernel<T, D, 16>), dim3(grid), dim3(256), 0, s, a);
+}
+
+int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_prefix, const void* v_prefix,
+             const int32_t* cu_prefix, const int32_t* prefix_len, const void* k_event, const void* v_event,
+             const int32_t* event_lens, const int32_t* cu_events, void* out, float* lse, void* workspace,
+             size_t workspace_bytes, void* stream)
+{
+    int rc = validate_dims(d, num_videos);
+    if (rc != PDEC_OK) return rc;
+    const void* ptrs[] = {q, k_event, v_event, out, workspace};
+    for (const void* p : ptrs)
+        if (!p || !aligned16(p)) return PDEC_ERR_INVALID_ARG;
+    // an empty prefix (max_prefix_len == 0) may come as null pointers
+    for (const void* p : {k_prefix, v_prefix})
+        if ((!p && d->max_prefix_len > 0) || !aligned16(p)) return PDEC_ERR_INVALID_ARG;
+    if (!event_lens || !aligned4(event_lens)) return PDEC_ERR_INVALID_ARG;
+    if (lse && !aligned4(lse)) return PDEC_ERR_INVALID_ARG;
+    if (cu_prefix) {
+        if (!cu_events || !aligned4(cu_prefix) || !aligned4(cu_events)) return PDEC_ERR_INVALID_ARG;
+    } else if (!prefix_len || !aligned4(prefix_len)) {
+        return PDEC_ERR_INVALID_ARG;
+    }
+    const Plan p = make_plan(d, num_videos);
+    if (workspace_bytes < p.ws_bytes) return PDEC_ERR_WORKSPACE;
+    if (p.n_prefix_items + p.n_tail_items > (long)INT32_MAX) return PDEC_ERR_UNSUPPORTED;
+
+    StepArgs a{};
+    a.q = q;
+    a.k_prefix = k_prefix;
+    a.v_prefix = v_prefix;
+    a.k_event = k_event;
+    a.v_event = v_event;
+    a.event_lens = event_lens;
+    a.cu_prefix = cu_prefix;
+    a.cu_events = cu_events;
+    a.prefix_len = cu_prefix ? nullptr : prefix_len;
+    a.out = out;
+    a.lse = lse;
+    const size_t rows = (size_t)d->num_events * d->num_q_heads;
+    a.part_o = static_cast<float*>(workspace);
+    a.part_m = a.part_o + (size_t)p.slots * rows * d->head_dim;
+    a.part_l = a.part_m + (size_t)p.slots * rows;
+    a.num_videos = num_videos;
+    a.num_events = d->num_events;
+    a.H_q = d->num_q_heads;
+    a.H_kv = d->num_kv_heads;
+    a.D = d->head_dim;
+    a.cap = d->event_cap;
+    a.G = d->num_q_heads / d->num_kv_heads;
+    a.chunk = p.chunk;
+    a.max_chunks = p.max_chunks;
+    a.rows_per_item = p.rows_per_item;
+    a.rg_max = p.rg_max;
+    a.tail_rg = p.tail_rg;
+    a.n_prefix_items = (int)p.n_prefix_items;
+    a.n_tail_items = (int)p.n_tail_items;
+    const float scale = d->softmax_scale > 0.f ? d->softmax_scale : 1.f / std::sqrt((float)d->head_dim);
+    a.qscale = scale * 1.4426950408889634f;
+
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int grid = (int)(p.n_prefix_items + p.n_tail_items);
+    const bool bf16 = d->dtype == PDEC_DTYPE_BF16;
+    const int timer_slot = g_timer_n > 0 ? (int)(g_timer_calls++ % g_timer_n) : -1;
+    if (timer_slot >= 0 && hipEventRecord(static_cast<hipEvent_t>(g_timer_start[timer_slot]), s) != hipSuccess)
+        return PDEC_ERR_HIP;
+    if (p.path == kPathMfma) {
+        if (d->head_dim == 128) launch_mfma<128>(a, p.nt, grid, s);
+        else launch_mfma<64>(a, p.nt, grid, s);
+    } else if (bf16) {
+        if (d->head_dim == 128) launch_valu<uint16_t, 128>(a, p.rows_per_item, grid, s);
+        else launch_valu<uint16_t, 64>(a, p.rows_per_item, grid, s);
+    } else {
+        if (d->head_dim == 128) launch_valu<float, 128>(a, p.rows_per_item, grid, s);
+        else launch_valu<float, 64>(a, p.rows_per_item, grid, s);
+    }
+    if ((rc = launch_status()) != PDEC_OK) return rc;
+    if (timer_slot >= 0 && hipEventRecord(static_cast<hipEvent_t>(g_timer_stop[timer_slot]), s) != hipSuccess)
+        return PDEC_ERR_HIP;
+    const int mgrid = (int)rows;
+    if (bf16) {
+        if (d->head_dim == 128) hipLaunchKernelGGL((merge_kernel<uint16_t, 128>), dim3(mgrid), dim3(64), 0, s, a);
+        else hipLaunchKernelGGL((merge_kernel<uint16_t, 64>), dim3(mgrid), dim3(64), 0, s, a);
+    } else {
+        if (d->head_dim == 128) hipLaunchKernelGGL((merge_kernel<float, 128>), dim3(mgrid), dim3(64), 0, s, a);
+        else hipLaunchKernelGGL((merge_kernel<float, 64>), dim3(mgrid), dim3(64), 0, s, a);
+    }
+    return launch_status();
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* pdec_strerror(int status)
+{
+    switch (status) {
+    case PDEC_OK: return "ok";
+    case PDEC_ERR_INVALID_ARG: return "invalid argument (null or misaligned pointer, inconsistent sizes)";
+    case PDEC_ERR_UNSUPPORTED: return "unsupported size or type (head_dim must be 64 or 128, dtype f32 or bf16)";
+    case PDEC_ERR_WORKSPACE: return "workspace smaller than pdec_workspace_size()";
+    case PDEC_ERR_HIP: return "HIP runtime error or kernel launch failure";
+    default: return "unknown pdec status";
+    }
+}
+
+size_t pdec_workspace_size(const pdec_dims* dims, int32_t num_videos)
+{
+    if (validate_dims(dims, num_videos) != PDEC_OK) return 0;
+    return make_plan(dims, num_videos).ws_bytes;
+}
+
+int pdec_attn_step(const pdec_dims* dims, const void* q, const void* k_prefix, const void* v_prefix,
+                   const void* k_event, const void* v_event, const int32_t* event_lens,
+                   const int32_t* prefix_lens, void* out, float* lse, void* workspace,
+                   size_t workspace_bytes, void* stream)
+{
+    return run_step(dims, 1, q, k_prefix, v_prefix, nullptr, prefix_lens, k_event, v_event, event_lens, nullptr,
+                    out, lse, workspace, workspace_bytes, stream);
+}
+
+int pdec_attn_step_ragged(const pdec_dims* dims, int32_t num_videos, const void* q, const void* k_prefix,
+                          const void* v_prefix, const int32_t* cu_prefix, const void* k_event,
+                          const void* v_event, const int32_t* event_lens, const int32_t* cu_events,
+                          void* out, float* lse, void* workspace, size_t workspace_bytes, void* stream)
+{
+    if (!cu_prefix || !cu_events) return PDEC_ERR_INVALID_ARG;
+    return run_step(dims, num_videos, q, k_prefix, v_prefix, cu_prefix, nullptr, k_event, v_event, event_lens,
+                    cu_events, out, lse, workspace, workspace_bytes, stream);
+}
+
+int pdec_kv_append(const pdec_dims* dims, const void* k_new, const void* v_new, void* k_event, void* v_event,
+                   int32_t* event_lens, const int32_t* live, void* stream)
+{
+    const int rc = validate_dims(dims, 1);
+    if (rc != PDEC_OK) return rc;
+    const void* ptrs[] = {k_new, v_new, k_event, v_event};
+    for (const void* p : ptrs)
+        if (!p || !aligned16(p)) return PDEC_ERR_INVALID_ARG;
+    if (!event_lens || !aligned4(event_lens)) return PDEC_ERR_INVALID_ARG;
+    if (live && !aligned4(live)) return PDEC_ERR_INVALID_ARG;
+    AppendArgs a{};
+    a.k_new = k_new;
+    a.v_new = v_new;
+    a.k_event = k_event;
+    a.v_event = v_event;
+    a.event_lens = event_lens;
+    a.live = live;
+    a.num_events = dims->num_events;
+    a.row_elems = dims->num_kv_heads * dims->head_dim;
+    a.cap = dims->event_cap;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (dims->dtype == PDEC_DTYPE_BF16)
+        hipLaunchKernelGGL((append_kernel<uint16_t>), dim3(a.num_events), dim3(256), 0, s, a);
+    else
+        hipLaunchKernelGGL((append_kernel<float>), dim3(a.num_events), dim3(256), 0, s, a);
+    return launch_status();
+}
+
+int pdec_set_path(int path)
+{
+    if (path < 0 || path > 2) return PDEC_ERR_INVALID_ARG;
+    return g_path_override.exchange(path);
+}
+
+int pdec_set_split_timer(void* const* start_events, void* const* stop_events, int n)
+{
+    if (n < 0) return PDEC_ERR_INVALID_ARG;
+    if (n > 0 && (!start_events || !stop_events)) return PDEC_ERR_INVALID_ARG;
+    g_timer_start = n > 0 ? start_events : nullptr;
+    g_timer_stop = n > 0 ? stop_events : nullptr;
+    g_timer_n = n;
+    g_timer_calls = 0;
+    return PDEC_OK;
+}
+
+int pdec_query_plan(const pdec_dims* dims, int32_t num_videos, int32_t* path, int32_t* chunk_keys)
+{
+    const int rc = validate_dims(dims, num_videos);
+    if (rc != PDEC_OK) return rc;
+    const Plan p = make_plan(dims, num_videos);
+    if (path) *path = p.path;
+    if (chunk_keys) *chunk_keys = p.chunk;
+    return PDEC_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,283 @@
+"""Python binding of libpdec (the C ABI of include/pdec.h) over ctypes.
+
+Argument marshalling only: tensors are checked for device, dtype, layout and
+shape, their device pointers and the current HIP stream are handed to the
+library, and every step of the computation runs in the library's kernels.
+PyTorch provides device memory and streams.  There is no fallback: if the
+built library is missing, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+from . import _build
+
+PDEC_OK = 0
+PDEC_ERR_INVALID_ARG = -1
+PDEC_ERR_UNSUPPORTED = -2
+PDEC_ERR_WORKSPACE = -3
+PDEC_ERR_HIP = -4
+PDEC_DTYPE_F32 = 0
+PDEC_DTYPE_BF16 = 1
+
+PATH_AUTO, PATH_VALU, PATH_MFMA = 0, 1, 2
+
+EXPORTED = ("pdec_strerror", "pdec_workspace_size", "pdec_attn_step", "pdec_attn_step_ragged",
+            "pdec_kv_append", "pdec_set_path", "pdec_query_plan", "pdec_set_split_timer")
+
+
+class Dims(ctypes.Structure):
+    """Mirror of ``pdec_dims``."""
+
+    _fields_ = [("num_events", ctypes.c_int32), ("num_q_heads", ctypes.c_int32),
+                ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("event_cap", ctypes.c_int32), ("max_prefix_len", ctypes.c_int32),
+                ("max_events_per_video", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("softmax_scale", ctypes.c_float)]
+
+
+class PdecError(RuntimeError):
+    def __init__(self, fn: str, code: int):
+        super().__init__(f"{fn} failed: {code} ({strerror(code)})")
+        self.code = code
+
+
+_lib = None
+
+
+def library_path() -> str:
+    return _build.LIBRARY
+
+
+def lib():
+    """The loaded libpdec; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        path = library_path()
+        if not os.path.exists(path):
+            raise RuntimeError(f"libpdec is not built ({path}); run __graft_entry__.build()")
+        L = ctypes.CDLL(path)
+        vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+        dp = ctypes.POINTER(Dims)
+        L.pdec_strerror.restype = ctypes.c_char_p
+        L.pdec_strerror.argtypes = [ctypes.c_int]
+        L.pdec_workspace_size.restype = sz
+        L.pdec_workspace_size.argtypes = [dp, i32]
+        L.pdec_attn_step.restype = ctypes.c_int
+        L.pdec_attn_step.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.pdec_attn_step_ragged.restype = ctypes.c_int
+        L.pdec_attn_step_ragged.argtypes = [dp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.pdec_kv_append.restype = ctypes.c_int
+        L.pdec_kv_append.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp]
+        L.pdec_set_path.restype = ctypes.c_int
+        L.pdec_set_path.argtypes = [ctypes.c_int]
+        L.pdec_query_plan.restype = ctypes.c_int
+        L.pdec_query_plan.argtypes = [dp, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)]
+        L.pdec_set_split_timer.restype = ctypes.c_int
+        L.pdec_set_split_timer.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int]
+        _lib = L
+    return _lib
+
+
+def strerror(code: int) -> str:
+    return lib().pdec_strerror(int(code)).decode()
+
+
+def _check(fn: str, rc: int):
+    if rc != PDEC_OK:
+        raise PdecError(fn, rc)
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return PDEC_DTYPE_BF16
+    if t.dtype == torch.float32:
+        return PDEC_DTYPE_F32
+    raise TypeError(f"pdec takes float32 or bfloat16 tensors, got {t.dtype}")
+
+
+def _dev(t: torch.Tensor, name: str, dtype=None, ndim=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be in device memory")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dims, got {tuple(t.shape)}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream, device) -> ctypes.c_void_p:
+    s = stream if stream is not None else torch.cuda.current_stream(device)
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def make_dims(num_events, H_q, H_kv, D, cap, max_prefix_len, dtype_code, scale=0.0,
+              max_events_per_video=0) -> Dims:
+    return Dims(int(num_events), int(H_q), int(H_kv), int(D), int(cap), int(max_prefix_len),
+                int(max_events_per_video), int(dtype_code), float(scale))
+
+
+def workspace_size(dims: Dims, num_videos: int = 1) -> int:
+    return int(lib().pdec_workspace_size(ctypes.byref(dims), int(num_videos)))
+
+
+def query_plan(dims: Dims, num_videos: int = 1):
+    """(path, chunk_keys) the library would use: path 1 = vector, 2 = matrix core."""
+    path, chunk = ctypes.c_int32(0), ctypes.c_int32(0)
+    _check("pdec_query_plan", lib().pdec_query_plan(ctypes.byref(dims), int(num_videos), ctypes.byref(path),
+                                                    ctypes.byref(chunk)))
+    return path.value, chunk.value
+
+
+def set_path(path: int) -> int:
+    """Force the split-pass kernel (0 auto, 1 vector, 2 matrix core); returns the previous value."""
+    rc = lib().pdec_set_path(int(path))
+    if rc < 0:
+        raise PdecError("pdec_set_path", rc)
+    return rc
+
+
+def _outputs(q, out, lse, workspace, ws_bytes):
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None:
+        lse = torch.empty(q.shape[0], q.shape[1], dtype=torch.float32, device=q.device)
+    if workspace is None:
+        workspace = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device=q.device)
+    return out, lse, workspace
+
+
+def attn_step(q, k_prefix, v_prefix, k_event, v_event, event_lens, prefix_lens, *, out=None, lse=None,
+              workspace=None, max_prefix_len=None, scale=0.0, stream=None, want_lse=True):
+    """One event-parallel decode step of one video; returns (out, lse).
+
+    q [E,H_q,D]; k/v_prefix [>=L,H_kv,D]; k/v_event [E,cap,H_kv,D];
+    event_lens int32 [E] (n_e incl. the current token, 0 = ended);
+    prefix_lens int32 [1] (device).  ``max_prefix_len`` bounds L (default:
+    the prefix tensors' row count).
+    """
+    E, H_q, D = q.shape
+    H_kv = k_prefix.shape[1]
+    cap = k_event.shape[1]
+    if max_prefix_len is None:
+        max_prefix_len = k_prefix.shape[0]
+    dims = make_dims(E, H_q, H_kv, D, cap, max_prefix_len, _dtype_code(q), scale)
+    ws_bytes = workspace_size(dims, 1)
+    out, lse, workspace = _outputs(q, out, lse, workspace, ws_bytes)
+    args = [_dev(q, "q", ndim=3), _dev(k_prefix, "k_prefix", q.dtype, 3), _dev(v_prefix, "v_prefix", q.dtype, 3),
+            _dev(k_event, "k_event", q.dtype, 4), _dev(v_event, "v_event", q.dtype, 4),
+            _dev(event_lens, "event_lens", torch.int32, 1), _dev(prefix_lens, "prefix_lens", torch.int32, 1),
+            _dev(out, "out", q.dtype, 3), _dev(lse, "lse", torch.float32, 2) if want_lse else None,
+            _dev(workspace, "workspace"), ctypes.c_size_t(workspace.numel() * workspace.element_size()),
+            _stream(stream, q.device)]
+    if v_prefix.shape != k_prefix.shape or v_event.shape != k_event.shape or k_event.shape[0] != E:
+        raise ValueError("inconsistent K/V shapes")
+    if k_prefix.shape[2] != D or k_event.shape[3] != D or k_event.shape[2] != H_kv:
+        raise ValueError("head dims disagree")
+    if event_lens.shape[0] != E or out.shape != q.shape:
+        raise ValueError("event_lens / out shape")
+    _check("pdec_attn_step", lib().pdec_attn_step(ctypes.byref(dims), *args))
+    return out, lse
+
+
+def attn_step_ragged(q, k_prefix, v_prefix, cu_prefix, k_event, v_event, event_lens, cu_events, *,
+                     max_prefix_len, max_events_per_video, out=None, lse=None, workspace=None, scale=0.0,
+                     stream=None, want_lse=True):
+    """One decode step over a ragged batch of videos; returns (out, lse).
+
+    k/v_prefix packed [sum L_v, H_kv, D]; cu_prefix, cu_events int32 [V+1]
+    (device); q/out [sum E_v, H_q, D]; k/v_event [sum E_v, cap, H_kv, D].
+    """
+    SE, H_q, D = q.shape
+    H_kv = k_prefix.shape[1]
+    cap = k_event.shape[1]
+    V = cu_prefix.shape[0] - 1
+    dims = make_dims(SE, H_q, H_kv, D, cap, max_prefix_len, _dtype_code(q), scale, max_events_per_video)
+    ws_bytes = workspace_size(dims, V)
+    out, lse, workspace = _outputs(q, out, lse, workspace, ws_bytes)
+    if cu_events.shape[0] != V + 1 or k_event.shape[0] != SE or event_lens.shape[0] != SE:
+        raise ValueError("inconsistent batch shapes")
+    if v_prefix.shape != k_prefix.shape or v_event.shape != k_event.shape or out.shape != q.shape:
+        raise ValueError("inconsistent K/V shapes")
+    args = [ctypes.c_int32(V), _dev(q, "q", ndim=3), _dev(k_prefix, "k_prefix", q.dtype, 3),
+            _dev(v_prefix, "v_prefix", q.dtype, 3), _dev(cu_prefix, "cu_prefix", torch.int32, 1),
+            _dev(k_event, "k_event", q.dtype, 4), _dev(v_event, "v_event", q.dtype, 4),
+            _dev(event_lens, "event_lens", torch.int32, 1), _dev(cu_events, "cu_events", torch.int32, 1),
+            _dev(out, "out", q.dtype, 3), _dev(lse, "lse", torch.float32, 2) if want_lse else None,
+            _dev(workspace, "workspace"), ctypes.c_size_t(workspace.numel() * workspace.element_size()),
+            _stream(stream, q.device)]
+    _check("pdec_attn_step_ragged", lib().pdec_attn_step_ragged(ctypes.byref(dims), *args))
+    return out, lse
+
+
+def kv_append(k_new, v_new, k_event, v_event, event_lens, live=None, *, stream=None):
+    """Append this step's K/V row of every live stream to its cache (in place).
+
+    k_new/v_new [E,H_kv,D]; k/v_event [E,cap,H_kv,D]; event_lens int32 [E]
+    (updated: n+1 for live streams, 0 for ended ones); live int32 [E] or None.
+    """
+    E, cap, H_kv, D = k_event.shape
+    dims = make_dims(E, H_kv, H_kv, D, cap, 0, _dtype_code(k_new))
+    if k_new.shape != (E, H_kv, D) or v_new.shape != k_new.shape or v_event.shape != k_event.shape:
+        raise ValueError("inconsistent append shapes")
+    args = [_dev(k_new, "k_new", None, 3), _dev(v_new, "v_new", k_new.dtype, 3),
+            _dev(k_event, "k_event", k_new.dtype, 4), _dev(v_event, "v_event", k_new.dtype, 4),
+            _dev(event_lens, "event_lens", torch.int32, 1),
+            None if live is None else _dev(live, "live", torch.int32, 1), _stream(stream, k_new.device)]
+    _check("pdec_kv_append", lib().pdec_kv_append(ctypes.byref(dims), *args))
+
+
+class SplitTimer:
+    """Times the split pass of the next step calls with HIP events.
+
+    Creates ``n`` pairs of hipEvent_t through the HIP runtime, hands them to
+    ``pdec_set_split_timer`` and, after the calls, returns each bracketed
+    kernel's duration.  The work done by the calls is unchanged.
+    """
+
+    def __init__(self, n: int):
+        self.n = int(n)
+        self._hip = ctypes.CDLL("libamdhip64.so")
+        self._hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self._hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        self._hip.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+        self._hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.start = (ctypes.c_void_p * self.n)()
+        self.stop = (ctypes.c_void_p * self.n)()
+        for arr in (self.start, self.stop):
+            for i in range(self.n):
+                ev = ctypes.c_void_p()
+                if self._hip.hipEventCreate(ctypes.byref(ev)) != 0:
+                    raise RuntimeError("hipEventCreate failed")
+                arr[i] = ev
+
+    def __enter__(self):
+        _check("pdec_set_split_timer", lib().pdec_set_split_timer(self.start, self.stop, self.n))
+        return self
+
+    def __exit__(self, *exc):
+        lib().pdec_set_split_timer(None, None, 0)
+
+    def durations_ms(self, count: int):
+        out = []
+        for i in range(min(count, self.n)):
+            self._hip.hipEventSynchronize(self.stop[i])
+            ms = ctypes.c_float()
+            if self._hip.hipEventElapsedTime(ctypes.byref(ms), self.start[i], self.stop[i]) != 0:
+                raise RuntimeError("hipEventElapsedTime failed")
+            out.append(ms.value)
+        return out
+
+    def close(self):
+        for arr in (self.start, self.stop):
+            for i in range(self.n):
+                if arr[i]:
+                    self._hip.hipEventDestroy(arr[i])
+                    arr[i] = None

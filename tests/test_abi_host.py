@@ -1,0 +1,102 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads, every
+entry point declared in include/pdec.h is exported, and the host planner and
+argument checks behave as documented."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2607_02963_amd import pdec
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    text = open(os.path.join(ROOT, "include", "pdec.h")).read()
+    return sorted(set(re.findall(r"\b(pdec_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = pdec.lib()
+    declared = _declared()
+    assert set(declared) == set(pdec.EXPORTED)
+    for name in declared:
+        assert hasattr(lib, name), name
+
+
+def _dims(**kw):
+    base = dict(num_events=32, H_q=28, H_kv=4, D=128, cap=129, max_prefix_len=32768,
+                dtype_code=pdec.PDEC_DTYPE_BF16)
+    base.update(kw)
+    return pdec.make_dims(base["num_events"], base["H_q"], base["H_kv"], base["D"], base["cap"],
+                          base["max_prefix_len"], base["dtype_code"])
+
+
+def test_strerror_covers_codes():
+    for c in (0, -1, -2, -3, -4, -99):
+        assert pdec.strerror(c)
+
+
+def test_workspace_size_rejects_bad_dims():
+    assert pdec.workspace_size(_dims(H_q=27)) == 0          # H_q % H_kv != 0
+    assert pdec.workspace_size(_dims(D=96)) == 0            # unsupported head dim
+    assert pdec.workspace_size(_dims(num_events=0)) == 0
+    assert pdec.workspace_size(_dims(cap=0)) == 0
+    assert pdec.workspace_size(_dims(dtype_code=7)) == 0
+    assert pdec.workspace_size(_dims(), num_videos=0) == 0
+
+
+def test_workspace_holds_every_partial_slot():
+    d = _dims()
+    path, chunk = pdec.query_plan(d)
+    slots = -(-32768 // chunk) + 1
+    assert pdec.workspace_size(d) == slots * 32 * 28 * (128 + 2) * 4
+    assert chunk % 128 == 0
+
+
+@pytest.mark.parametrize("E,G,dt,expect", [(32, 7, pdec.PDEC_DTYPE_BF16, pdec.PATH_MFMA),
+                                            (1, 7, pdec.PDEC_DTYPE_BF16, pdec.PATH_VALU),
+                                            (3, 7, pdec.PDEC_DTYPE_BF16, pdec.PATH_MFMA),
+                                            (2, 7, pdec.PDEC_DTYPE_BF16, pdec.PATH_VALU),
+                                            (4, 4, pdec.PDEC_DTYPE_F32, pdec.PATH_VALU)])
+def test_dispatch_rule(E, G, dt, expect):
+    """bf16 with >= 16 query rows per kv head -> matrix core, else vector ALUs."""
+    d = _dims(num_events=E, H_q=G, H_kv=1, dtype_code=dt)
+    assert pdec.query_plan(d)[0] == expect
+
+
+def test_path_override_round_trip():
+    prev = pdec.set_path(pdec.PATH_VALU)
+    try:
+        assert pdec.query_plan(_dims())[0] == pdec.PATH_VALU
+    finally:
+        pdec.set_path(prev)
+    assert pdec.query_plan(_dims())[0] == pdec.PATH_MFMA
+    with pytest.raises(pdec.PdecError):
+        pdec.set_path(5)
+
+
+def test_step_rejects_bad_arguments_before_any_launch():
+    """Null / misaligned pointers and a short workspace fail on the host.
+    Every call here is rejected before anything is enqueued (the fake
+    pointers are never dereferenced)."""
+    L = pdec.lib()
+    d = _dims()
+    ws = pdec.workspace_size(d)
+    good = ctypes.c_void_p(0x10000)
+    args = [good] * 9 + [good, ctypes.c_size_t(ws), None]
+    bad_null = list(args)
+    bad_null[0] = None
+    assert L.pdec_attn_step(ctypes.byref(d), *bad_null) == pdec.PDEC_ERR_INVALID_ARG
+    bad_align = list(args)
+    bad_align[1] = ctypes.c_void_p(0x10008)
+    assert L.pdec_attn_step(ctypes.byref(d), *bad_align) == pdec.PDEC_ERR_INVALID_ARG
+    short = list(args)
+    short[10] = ctypes.c_size_t(ws - 4)
+    assert L.pdec_attn_step(ctypes.byref(d), *short) == pdec.PDEC_ERR_WORKSPACE
+    bad_dims = _dims(D=80)
+    assert L.pdec_attn_step(ctypes.byref(bad_dims), *args) == pdec.PDEC_ERR_UNSUPPORTED
+    assert L.pdec_attn_step_ragged(ctypes.byref(d), 1, *([good] * 3), None, *([good] * 3), None,
+                                   good, good, good, ctypes.c_size_t(ws), None) == pdec.PDEC_ERR_INVALID_ARG
+    assert L.pdec_kv_append(ctypes.byref(d), None, good, good, good, good, None, None) == pdec.PDEC_ERR_INVALID_ARG
