@@ -67,9 +67,12 @@ typedef struct pdec_dims {
     int32_t head_dim;             /* D: 64 or 128                                                */
     int32_t event_cap;            /* rows per stream cache, >= 1                                 */
     int32_t max_prefix_len;       /* upper bound on any video's prefix length, >= 0              */
-    int32_t max_events_per_video; /* upper bound on streams in one video; 0 means num_events     */
+    int32_t max_events_per_video; /* upper bound on streams in one video (<= 2048); 0 means      */
+                                  /* min(num_events, 2048)                                       */
     int32_t dtype;                /* pdec_dtype of q, k, v and out                               */
     float softmax_scale;          /* <= 0 selects 1/sqrt(head_dim)                               */
+    int64_t prefix_tokens;        /* prefix rows over the whole batch (sizing hint for the work  */
+                                  /* split); 0 means num_videos * max_prefix_len                 */
 } pdec_dims;
 
 /* Human-readable text of a pdec_status code.  Never NULL. */

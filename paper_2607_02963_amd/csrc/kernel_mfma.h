@@ -1,34 +1,42 @@
 // Matrix-core split pass (bf16, >= 16 query rows per kv head).
 //
-// The prefix part of the step is a dense contraction: for one kv head, all
-// R = E*G query rows of a video against every key of the shared prefix
-// (§3.4, Eq. 3).  Each prefix K/V element is read once from HBM and used by
-// all R rows.
+// The prefix part of a step is a dense contraction: for one kv head, every
+// query row of a video (R = E*G of them) against every key of the shared
+// prefix (§3.4, Eq. 3).  One work-group takes one chunk of the virtual key
+// sequence (prefix units, then each stream's own units; see pdec_common.h)
+// for up to 256 rows, so each prefix K/V byte is fetched from HBM once and
+// used by all of those rows; an own unit of stream f is used by f's rows
+// only.
 //
-// Work-group = 4 waves; the item's rows (NT tiles of 16) are held by every
-// wave, and the item's keys are dealt to the waves in 32-key sub-blocks
-// (wave w takes keys [128 b + 32 w, 128 b + 32 w + 32) of block b).  Waves
-// never synchronise inside the key loop; at the end their partial states are
-// merged through LDS.
+// Work-group: 8 waves = WR row waves x WK key groups.  Row wave rw owns NT
+// 16-row tiles; key group kg owns a contiguous 64/WK-key slice of every
+// 64-key stage (one unit).  Keys stream through a 4-stage LDS ring filled by
+// global_load_lds_dwordx4 (direct HBM -> LDS DMA, 1 KB per wave
+// instruction, no staging registers), three stages in flight while the
+// fourth is consumed.  Each key row (D bf16) is stored as D/8 16-byte chunks
+// permuted by an XOR of the key index, so the matrix-core operand reads below
+// hit distinct LDS banks.
 //
-// Per 32-key sub-block, with v_mfma_f32_16x16x32_bf16 (D = A(16x32) B(32x16)):
-//   S^T  = K  Q^T    A = K rows (16 keys x 32 d), B = Q^T (32 d x 16 rows)
-//   O^T += V^T P^T   A = V^T (16 d x 32 keys),   B = P^T (32 keys x 16 rows)
+// Per 32-key block, with v_mfma_f32_16x16x32_bf16 (D = A(16x32) B(32x16)):
+//   S^T  = K  Q^T    A = K rows from LDS (16 keys x 32 d), B = Q^T (registers)
+//   O^T += V^T P^T   A = V^T via ds_read_b64_tr_b16, B = P^T (registers)
 // The S^T accumulator gives lane l the scores of query row l%16 for keys
 // 4(l/16)..+3 of each 16-key tile, which is exactly a B operand of the second
-// product once converted to bf16; so P never leaves registers, and O^T's
-// accumulator holds the same query row in the same lane as that row's softmax
-// state.  V must have the key as its contraction index: it is written
-// transposed into a per-wave LDS tile and read back 8 keys at a time.  For
-// both products the k-index order inside a lane only has to agree between A
-// and B, which it does by construction.
+// product once rounded to bf16, so P never leaves registers and O^T holds
+// that query row in the same lane as its softmax state.  The transposing LDS
+// read hands lane l the values of d = l%16 for four consecutive keys, which
+// is the A operand of V^T with the same key order as P^T.
 //
-// Softmax: base-2, the q scale folded into the exponent
-// (p = 2^(s*c - m)).  The running reference max m is raised only when a tile
-// max exceeds it by more than 8 (then O and l are rescaled); otherwise
-// p <= 2^8, exact in the final ratio.  Keys past the item are masked to -inf
-// and their V rows are zero-filled, never loaded.
+// Softmax in base 2 with the q scale folded into the exponent
+// (p = 2^(s*c - m)).  Each row keeps a reference max m, raised only when that
+// row's block max exceeds it by more than 8 (then its O and l are rescaled);
+// otherwise p <= 2^8 and the final ratio is exact.  A row's arithmetic never
+// depends on another row's values.  Keys past a unit's valid count, and own
+// units of other streams, are masked to -inf; DMA reads are clamped to the
+// unit's last valid key, so nothing outside it is ever fetched.
 #pragma once
+
+#include <type_traits>
 
 #include "pdec_common.h"
 
@@ -37,6 +45,10 @@ namespace pdec {
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
 typedef __attribute__((ext_vector_type(4))) float f32x4_t;
 typedef __attribute__((ext_vector_type(4))) uint32_t u32x4_t;
+typedef __attribute__((ext_vector_type(2))) uint32_t u32x2_t;
+typedef __attribute__((ext_vector_type(4))) short s16x4_t;
+
+typedef __attribute__((address_space(3))) void lds_void_t;
 
 __device__ inline f32x4_t mfma_16x16x32(bf16x8_t a, bf16x8_t b, f32x4_t c)
 {
@@ -51,274 +63,391 @@ __device__ inline uint32_t pack_bf16x2(float lo, float hi)
     return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
 }
 
-template <int D, int NT>
-__global__ __launch_bounds__(256) void split_mfma_kernel(StepArgs a)
+// Reductions over the 4 lane groups (lanes l, l^16, l^32, l^48) that hold one
+// query row in the S^T accumulator layout.  v_permlane16_swap exchanges odd
+// 16-lane rows of one operand with even rows of the other, v_permlane32_swap
+// the upper half of one with the lower half of the other; with the value in
+// both operands the two results hold the partner groups' values.  Plain VALU
+// instructions: no LDS traffic.
+__device__ inline float max_over_groups(float x)
 {
-    constexpr int NW = 4;               // waves per work-group
-    constexpr int KSUB = 32;            // keys per wave per block
-    constexpr int KBLK = NW * KSUB;     // keys per block
-    constexpr int KSTEPS = D / 32;      // k-steps of S^T = K Q^T
-    constexpr int DT = D / 16;          // 16-row d tiles of O^T
-    constexpr int VCH = KSUB * D / 8 / 64;  // 16-byte V chunks per lane per sub-block
-    constexpr int VTS = KSUB + 8;       // LDS row stride (bf16) of the V^T tile
-    constexpr int OROW = D + 4;         // LDS row stride (floats) of the merge buffer
-    constexpr int LDS_VT = NW * D * VTS * 2;
-    constexpr int LDS_MERGE = 2 * NT * 16 * OROW * 4 + 2 * NW * NT * 16 * 4;
-    constexpr int LDS_BYTES = LDS_VT > LDS_MERGE ? LDS_VT : LDS_MERGE;
-    __shared__ __attribute__((aligned(16))) unsigned char lds[LDS_BYTES];
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    const float y = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(y), __float_as_uint(y), false, false);
+    return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ inline float sum_over_groups(float x)
+{
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    const float y = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(y), __float_as_uint(y), false, false);
+    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
 
-    Item it;
-    if (!decode_item(a, blockIdx.x, it)) return;
+// Initial reference max: finite, so no -inf special cases are needed; the
+// first block with any visible key always re-references (its max exceeds
+// this by more than 8), and 2^(s*c - kMinRef) is never evaluated before.
+constexpr float kMinRef = -1e30f;
+
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
+template <int N>
+__device__ inline void wait_vmcnt()
+{
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// LDS byte address of a pointer into a __shared__ array.
+__device__ inline uint32_t lds_u32(const void* p) { return (uint32_t)(uintptr_t)(lds_void_t*)p; }
+
+// One wave-wide 16-byte-per-lane DMA from global memory straight into LDS:
+// lane l's 16 bytes land at lds_base + 16 l.  Issued from inline assembly so
+// the compiler does not pair it with a conservative drain of every
+// outstanding load before later LDS reads; completion is awaited explicitly
+// with stage_barrier.  M0 (the LDS base register) is restored afterwards.
+__device__ inline void dma_16B(const void* src, uint32_t lds_base)
+{
+    uint32_t saved;
+    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %2, off\n\ts_mov_b32 m0, %0"
+                 : "=&s"(saved)
+                 : "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(src)
+                 : "memory");
+}
+
+// Wait until at most N of this wave's vector-memory operations are in flight
+// and its LDS operations are done, then barrier the work-group.  Written as
+// one asm statement so the compiler neither drains every DMA nor moves LDS
+// accesses across it.
+template <int N>
+__device__ inline void stage_barrier()
+{
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
+}
+
+template <int D, int NT, int WR, int WK>
+struct MfmaCfg {
+    static constexpr int NW = WR * WK;            // waves
+    static constexpr int KS = kUnit;              // keys per stage: one unit
+    static constexpr int KW = KS / WK;            // keys per key group per stage
+    static constexpr int NSTAGE = 4;
+    static constexpr int ROWB = D * 2;            // bytes per key row
+    static constexpr int CH = D / 8;              // 16-byte chunks per key row
+    static constexpr int STAGE_K = KS * ROWB;     // bytes of K per stage
+    static constexpr int STAGE = 2 * STAGE_K;     // K then V
+    static constexpr int KPI = 1024 / ROWB;       // keys per 1 KB DMA instruction
+    static constexpr int DMA_PER_STAGE = STAGE / 1024;
+    static constexpr int DMA_PER_WAVE = DMA_PER_STAGE / NW;
+    static constexpr int KSTEPS = D / 32;
+    static constexpr int DT = D / 16;
+    static constexpr int RT = 16 * NT * WR;       // rows per item
+    static constexpr int LDS = NSTAGE * STAGE;
+    static_assert(NW == 8, "eight waves");
+    static_assert(KW % 32 == 0, "key group slice is whole 32-key blocks");
+    static_assert(DMA_PER_STAGE % NW == 0, "DMA split");
+    // cross-key-group merge buffer fits in the ring
+    static_assert(WK == 1 || (WR * NT * 16 * (D + 4) * 4 + 2 * WR * NT * 16 * 4) <= LDS, "merge buffer");
+};
+
+// Byte offset of 16-byte chunk `ch` of key `key` inside a stage's K or V area.
+template <int D>
+__device__ inline int k_off(int key, int ch) { return key * (2 * D) + 16 * (ch ^ (key % (D / 8))); }
+template <int D>
+__device__ inline int v_off(int key, int ch) { return key * (2 * D) + 16 * (ch ^ ((2 * key) & 6)); }
+
+template <int D, int NT, int WR, int WK>
+__global__ __launch_bounds__(512) void split_mfma_kernel(StepArgs a)
+{
+    using C = MfmaCfg<D, NT, WR, WK>;
+    __shared__ __attribute__((aligned(1024))) unsigned char lds[C::LDS];
+    __shared__ int tab_start[kMaxStreamsPerVideo + 1];
+    __shared__ int tab_nlen[kMaxStreamsPerVideo];
+    __shared__ int s_total;
+
+    // ---- which item; every branch below is uniform over the work-group ----
+    const int item = item_of_block(a, blockIdx.x);
+    if (item < 0) return;
+    const ItemId id = item_id(a, item);
+    const VideoInfo vi = video_info(a, id.v);
+    const int R = vi.E * a.G;
+    const int row0 = id.rg * C::RT;
+    if (row0 >= R) return;
+    const int nrows = min(C::RT, R - row0);
 
     const int tid = threadIdx.x;
     const int w = tid >> 6;
     const int lane = tid & 63;
-    const int l16 = lane & 15;  // row (N) / key-in-tile (M) index inside a 16-tile
-    const int lg = lane >> 4;   // lane group: selects the k sub-range
+    const int l16 = lane & 15;
+    const int lg = lane >> 4;
+    const int rw = w % WR;
+    const int kg = w / WR;
     const float c = a.qscale;
 
-    const uint16_t* __restrict__ kp = static_cast<const uint16_t*>(it.prefix ? a.k_prefix : a.k_event) + it.key_off;
-    const uint16_t* __restrict__ vp = static_cast<const uint16_t*>(it.prefix ? a.v_prefix : a.v_event) + it.key_off;
+    const int upre = (vi.L + kUnit - 1) / kUnit;
+    const int upc = a.unit_per_chunk;
+    const int u0 = id.c * upc;
+    const bool first_item = id.c == 0 && id.g == 0 && id.rg == 0;
+    int u1 = u0 + upc;
+    if (u1 > upre || first_item) {  // reaches own units, or reports the chunk count
+        if (w == 0) {
+            const int own = build_unit_table(a, vi, tab_start, tab_nlen);
+            if (lane == 0) s_total = upre + own;
+        }
+        lds_barrier();
+        const int total = s_total;
+        if (first_item && tid == 0) a.video_chunks[id.v] = min(max((total + upc - 1) / upc, 1), a.max_chunks);
+        u1 = min(u1, total);
+    }
+    if (u0 >= u1) return;
+    const int nstages = u1 - u0;
+
+    const uint16_t* __restrict__ kpre = static_cast<const uint16_t*>(a.k_prefix);
+    const uint16_t* __restrict__ vpre = static_cast<const uint16_t*>(a.v_prefix);
+    const uint16_t* __restrict__ kev = static_cast<const uint16_t*>(a.k_event);
+    const uint16_t* __restrict__ vev = static_cast<const uint16_t*>(a.v_event);
     const long stride = (long)a.H_kv * D;
 
-    // Q^T operands: lane holds q[row 16nt + l16][32t + 8lg .. +7], zero for padding rows.
-    bf16x8_t qf[NT][KSTEPS];
+    // rows of this lane: 16*(rw*NT+nt) + l16 within the item, stream-major
+    const int wrow0 = row0 + 16 * rw * NT;                // first video row of this wave
+    const bool row_wave_active = 16 * rw * NT < nrows;
+    int lane_stream[NT];
+    bf16x8_t qf[NT][C::KSTEPS];  // Q^T operands: q[row][32t + 8lg .. +7]
     {
         const uint16_t* __restrict__ q = static_cast<const uint16_t*>(a.q);
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
-            const int r = 16 * nt + l16;
-            const bool ok = r < it.nrows;
-            const long base = ok ? (long)item_qrow(a, it, r) * D : 0;
+            const int r = 16 * (rw * NT + nt) + l16;
+            const bool ok = r < nrows;
+            lane_stream[nt] = ok ? (row0 + r) / a.G : -2;
+            const long base = ok ? (long)row_qrow(a, vi, id.g, row0 + r) * D : 0;
 #pragma unroll
-            for (int t = 0; t < KSTEPS; ++t) {
+            for (int t = 0; t < C::KSTEPS; ++t) {
                 u32x4_t x = {0u, 0u, 0u, 0u};
                 if (ok) x = *reinterpret_cast<const u32x4_t*>(q + base + 32 * t + 8 * lg);
                 qf[nt][t] = as_bf16x8(x);
             }
         }
     }
+    wait_vmcnt<0>();
 
-    f32x4_t o[NT][DT];
+    // DMA of one stage (unit u0 + st): this wave's DMA_PER_WAVE 1 KB pieces.
+    // Piece p covers KPI keys of K (p < DMA_PER_STAGE/2) or of V; lane l
+    // moves chunk (l % CH) ^ swizzle(key) of key (l / CH) of the piece, so the
+    // piece lands in LDS already permuted.
+    auto issue_stage = [&](int st) {
+        const UnitInfo ui = unit_info(a, vi, upre, tab_start, tab_nlen, id.g, u0 + st);
+        const uint16_t* kb = (ui.stream < 0 ? kpre : kev) + ui.key_off;
+        const uint16_t* vb = (ui.stream < 0 ? vpre : vev) + ui.key_off;
+        unsigned char* sbase = lds + (st % C::NSTAGE) * C::STAGE;
+#pragma unroll
+        for (int i = 0; i < C::DMA_PER_WAVE; ++i) {
+            const int piece = w * C::DMA_PER_WAVE + i;
+            const bool is_v = piece >= C::DMA_PER_STAGE / 2;
+            const int pk = is_v ? piece - C::DMA_PER_STAGE / 2 : piece;
+            const int key = pk * C::KPI + lane / C::CH;
+            const int slot = lane % C::CH;
+            const int ch = is_v ? (slot ^ ((2 * key) & 6)) : (slot ^ (key % C::CH));
+            const int gkey = min(key, ui.nk - 1);
+            const uint16_t* src = (is_v ? vb : kb) + (long)gkey * stride + 8 * ch;
+            unsigned char* dst = sbase + (is_v ? C::STAGE_K : 0) + pk * 1024;
+            dma_16B(src, lds_u32(dst));
+        }
+    };
+
+    f32x4_t o[NT][C::DT];
     float m_ref[NT], l_part[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-        m_ref[nt] = kNegInf;
+        m_ref[nt] = kMinRef;
         l_part[nt] = 0.f;
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) o[nt][dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        for (int dt = 0; dt < C::DT; ++dt) o[nt][dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     }
 
-    uint16_t* vt = reinterpret_cast<uint16_t*>(lds) + w * D * VTS;
-    const int nblocks = (it.nkeys + KBLK - 1) / KBLK;
+    // Per-lane LDS byte offsets of the operand reads, relative to the first
+    // key of a 16-key group (the XOR swizzle depends on the lane only).
+    //  K: key 16kt + l16, chunk 4t + lg.
+    //  V: key 4lg + l16/4 (+16), d = 16dt + 4(l16 % 4) .. +3 (8 bytes).
+    int koff[C::KSTEPS], voff[C::DT];
+#pragma unroll
+    for (int t = 0; t < C::KSTEPS; ++t) koff[t] = l16 * C::ROWB + 16 * ((4 * t + lg) ^ (l16 % C::CH));
+#pragma unroll
+    for (int dt = 0; dt < C::DT; ++dt) {
+        const int key = 4 * lg + (l16 >> 2);
+        const int ch = 2 * dt + ((l16 & 3) >> 1);
+        voff[dt] = key * C::ROWB + 16 * (ch ^ (2 * (key & 3))) + 8 * (l16 & 1);
+    }
 
-    u32x4_t kr[2][KSTEPS], vr[VCH];
-    auto load_block = [&](int b) {
-        const int kb = b * KBLK + w * KSUB;
+    // One 32-key block of this wave: S^T, online softmax, O^T += V^T P^T.
+    // MASKED: keys past nk and, for an own unit, rows of other streams are
+    // excluded; the unmasked form serves every full prefix unit.
+    auto block = [&](auto masked_tag, const unsigned char* kbuf, const unsigned char* vbuf, int kb,
+                     const UnitInfo& ui) {
+        constexpr bool MASKED = decltype(masked_tag)::value;
+        f32x4_t s[2][NT];
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt) {
-            const int key = kb + 16 * kt + l16;
-            const bool ok = key < it.nkeys;
 #pragma unroll
-            for (int t = 0; t < KSTEPS; ++t) {
-                u32x4_t x = {0u, 0u, 0u, 0u};
-                if (ok) x = *reinterpret_cast<const u32x4_t*>(kp + (long)key * stride + 32 * t + 8 * lg);
-                kr[kt][t] = x;
+            for (int nt = 0; nt < NT; ++nt) s[kt][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int t = 0; t < C::KSTEPS; ++t) {
+                const bf16x8_t kf =
+                    as_bf16x8(*reinterpret_cast<const u32x4_t*>(kbuf + (kb + 16 * kt) * C::ROWB + koff[t]));
+#pragma unroll
+                for (int nt = 0; nt < NT; ++nt) s[kt][nt] = mfma_16x16x32(kf, qf[nt][t], s[kt][nt]);
             }
         }
-#pragma unroll
-        for (int i = 0; i < VCH; ++i) {
-            const int ch = i * 64 + lane;
-            const int key = kb + ch / (D / 8);
-            const int d0 = 8 * (ch % (D / 8));
-            u32x4_t x = {0u, 0u, 0u, 0u};
-            if (key < it.nkeys) x = *reinterpret_cast<const u32x4_t*>(vp + (long)key * stride + d0);
-            vr[i] = x;
-        }
-    };
-
-    if (nblocks > 0) load_block(0);
-    for (int b = 0; b < nblocks; ++b) {
-        const int kb = b * KBLK + w * KSUB;
-        // V^T into this wave's LDS tile; key k = 16 kt + 4 j + i sits at column 8 j + 4 kt + i
-#pragma unroll
-        for (int i = 0; i < VCH; ++i) {
-            const int ch = i * 64 + lane;
-            const int k = ch / (D / 8);
-            const int d0 = 8 * (ch % (D / 8));
-            const int col = 8 * ((k & 15) >> 2) + 4 * (k >> 4) + (k & 3);
-            const uint32_t words[4] = {vr[i].x, vr[i].y, vr[i].z, vr[i].w};
-#pragma unroll
-            for (int x = 0; x < 4; ++x) {
-                vt[(d0 + 2 * x) * VTS + col] = (uint16_t)(words[x] & 0xffffu);
-                vt[(d0 + 2 * x + 1) * VTS + col] = (uint16_t)(words[x] >> 16);
-            }
-        }
-        bf16x8_t kf[2][KSTEPS];
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-            for (int t = 0; t < KSTEPS; ++t) kf[kt][t] = as_bf16x8(kr[kt][t]);
-        if (b + 1 < nblocks) load_block(b + 1);
-
-        if (kb < it.nkeys) {
-            // S^T for the two 16-key tiles and every row tile
-            f32x4_t s[2][NT];
+        if constexpr (MASKED) {
 #pragma unroll
             for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-                for (int nt = 0; nt < NT; ++nt) {
-                    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+                for (int i = 0; i < 4; ++i) {
+                    const bool kout = kb + 16 * kt + 4 * lg + i >= ui.nk;
 #pragma unroll
-                    for (int t = 0; t < KSTEPS; ++t) acc = mfma_16x16x32(kf[kt][t], qf[nt][t], acc);
-                    s[kt][nt] = acc;
+                    for (int nt = 0; nt < NT; ++nt)
+                        if (kout || (ui.stream >= 0 && lane_stream[nt] != ui.stream)) s[kt][nt][i] = kNegInf;
                 }
-            // mask keys past the item
-            if (kb + KSUB > it.nkeys) {
-#pragma unroll
-                for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        if (kb + 16 * kt + 4 * lg + i >= it.nkeys) {
-#pragma unroll
-                            for (int nt = 0; nt < NT; ++nt) s[kt][nt][i] = kNegInf;
-                        }
-                    }
-            }
-            // tile max per row (raw score units), shared by the row's 4 lanes
-            float mt[NT];
-            bool need = false;
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt) {
-                float mx = fmaxf(fmaxf(fmaxf(s[0][nt][0], s[0][nt][1]), fmaxf(s[0][nt][2], s[0][nt][3])),
-                                 fmaxf(fmaxf(s[1][nt][0], s[1][nt][1]), fmaxf(s[1][nt][2], s[1][nt][3])));
-                mx = fmaxf(mx, __shfl_xor(mx, 16));
-                mx = fmaxf(mx, __shfl_xor(mx, 32));
-                mt[nt] = mx * c;
-                need |= mt[nt] > m_ref[nt] + 8.f;
-            }
-            if (__any(need)) {
-                // rows whose own max moved up by more than 8 take the new
-                // reference; every other row keeps its reference (alpha = 1,
-                // exact), so a row's arithmetic never depends on other rows
-#pragma unroll
-                for (int nt = 0; nt < NT; ++nt) {
-                    const bool up = mt[nt] > m_ref[nt] + 8.f;
-                    const float mnew = up ? mt[nt] : m_ref[nt];
-                    const float alpha = (up && m_ref[nt] != kNegInf) ? fast_exp2(m_ref[nt] - mnew) : 1.f;
-                    m_ref[nt] = mnew;
-                    l_part[nt] *= alpha;
-#pragma unroll
-                    for (int dt = 0; dt < DT; ++dt) o[nt][dt] *= alpha;
-                }
-            }
-            // P^T operands (bf16) and the normaliser
-            bf16x8_t pf[NT];
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt) {
-                const float mr = m_ref[nt] == kNegInf ? 0.f : m_ref[nt];
-                float p[8];
-#pragma unroll
-                for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) p[4 * kt + i] = fast_exp2(fmaf(s[kt][nt][i], c, -mr));
-                float sum = 0.f;
-#pragma unroll
-                for (int i = 0; i < 8; ++i) sum += p[i];
-                l_part[nt] += sum;
-                u32x4_t pk = {pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]),
-                              pack_bf16x2(p[6], p[7])};
-                pf[nt] = as_bf16x8(pk);
-            }
-            __builtin_amdgcn_wave_barrier();
-            // O^T += V^T P^T
-#pragma unroll
-            for (int dt = 0; dt < DT; ++dt) {
-                const u32x4_t vx = *reinterpret_cast<const u32x4_t*>(vt + (16 * dt + l16) * VTS + 8 * lg);
-                const bf16x8_t vf = as_bf16x8(vx);
-#pragma unroll
-                for (int nt = 0; nt < NT; ++nt) o[nt][dt] = mfma_16x16x32(vf, pf[nt], o[nt][dt]);
-            }
         }
-        __builtin_amdgcn_wave_barrier();
-    }
-
-    // normaliser: sum the 4 lane groups of each row
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-        l_part[nt] += __shfl_xor(l_part[nt], 16);
-        l_part[nt] += __shfl_xor(l_part[nt], 32);
-    }
-
-    // ---- merge the 4 waves' states through LDS ----
-    __syncthreads();  // every wave is done with its V^T tile
-    float* obuf0 = reinterpret_cast<float*>(lds);
-    float* obuf1 = obuf0 + NT * 16 * OROW;
-    float* mbuf = obuf1 + NT * 16 * OROW;  // [NW][NT*16]
-    float* lbuf = mbuf + NW * NT * 16;     // [NW][NT*16]
-    if (lg == 0) {
+        // block max per row; rows whose max rose by more than 8 re-reference
+        float mt[NT];
+        bool need = false;
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
-            mbuf[w * NT * 16 + 16 * nt + l16] = m_ref[nt];
-            lbuf[w * NT * 16 + 16 * nt + l16] = l_part[nt];
+            const float mx = fmaxf(fmaxf(fmaxf(s[0][nt][0], s[0][nt][1]), fmaxf(s[0][nt][2], s[0][nt][3])),
+                                   fmaxf(fmaxf(s[1][nt][0], s[1][nt][1]), fmaxf(s[1][nt][2], s[1][nt][3])));
+            mt[nt] = max_over_groups(mx) * c;
+            need |= mt[nt] > m_ref[nt] + 8.f;
         }
-    }
-    __syncthreads();
-    float mall[NT], lall[NT];
+        if (__any(need)) {
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-        float M = kNegInf;
+            for (int nt = 0; nt < NT; ++nt) {
+                const bool up = mt[nt] > m_ref[nt] + 8.f;
+                const float alpha = up ? fast_exp2(m_ref[nt] - mt[nt]) : 1.f;
+                m_ref[nt] = up ? mt[nt] : m_ref[nt];
+                l_part[nt] *= alpha;
 #pragma unroll
-        for (int ww = 0; ww < NW; ++ww) M = fmaxf(M, mbuf[ww * NT * 16 + 16 * nt + l16]);
-        float L = 0.f;
-#pragma unroll
-        for (int ww = 0; ww < NW; ++ww) {
-            const float mw = mbuf[ww * NT * 16 + 16 * nt + l16];
-            L += (mw == kNegInf ? 0.f : fast_exp2(mw - M)) * lbuf[ww * NT * 16 + 16 * nt + l16];
+                for (int dt = 0; dt < C::DT; ++dt) o[nt][dt] *= alpha;
+            }
         }
-        mall[nt] = M;
-        lall[nt] = L;
-        const float f = m_ref[nt] == kNegInf ? 0.f : fast_exp2(m_ref[nt] - M);
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) o[nt][dt] *= f;
-    }
-    auto store_o = [&](float* buf) {
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-            for (int dt = 0; dt < DT; ++dt)
-                *reinterpret_cast<f32x4_t*>(buf + (16 * nt + l16) * OROW + 16 * dt + 4 * lg) = o[nt][dt];
-    };
-    auto add_o = [&](const float* buf) {
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-            for (int dt = 0; dt < DT; ++dt)
-                o[nt][dt] += *reinterpret_cast<const f32x4_t*>(buf + (16 * nt + l16) * OROW + 16 * dt + 4 * lg);
-    };
-    if (w == 2) store_o(obuf0);
-    if (w == 3) store_o(obuf1);
-    __syncthreads();
-    if (w == 0) add_o(obuf0);
-    if (w == 1) add_o(obuf1);
-    __syncthreads();
-    if (w == 1) store_o(obuf0);
-    __syncthreads();
-    if (w == 0) {
-        add_o(obuf0);
-        const long SEH = (long)a.num_events * a.H_q;
+        bf16x8_t pf[NT];
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
-            const int r = 16 * nt + l16;
-            if (r < it.nrows) {
-                const long qr = item_qrow(a, it, r);
-                float* dst = a.part_o + ((long)it.slot * SEH + qr) * D;
+            float p[8];
 #pragma unroll
-                for (int dt = 0; dt < DT; ++dt) *reinterpret_cast<f32x4_t*>(dst + 16 * dt + 4 * lg) = o[nt][dt];
+            for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) p[4 * kt + i] = fast_exp2(fmaf(s[kt][nt][i], c, -m_ref[nt]));
+            l_part[nt] += ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
+            const u32x4_t pk = {pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]),
+                                pack_bf16x2(p[6], p[7])};
+            pf[nt] = as_bf16x8(pk);
+        }
+#pragma unroll
+        for (int dt = 0; dt < C::DT; ++dt) {
+            const unsigned char* va = vbuf + kb * C::ROWB + voff[dt];
+            const s16x4_t x0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4_t*)va);
+            const s16x4_t x1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (__attribute__((address_space(3))) s16x4_t*)(va + 16 * C::ROWB));
+            const u32x2_t xa = __builtin_bit_cast(u32x2_t, x0);
+            const u32x2_t xb = __builtin_bit_cast(u32x2_t, x1);
+            const bf16x8_t vf = as_bf16x8(u32x4_t{xa.x, xa.y, xb.x, xb.y});
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) o[nt][dt] = mfma_16x16x32(vf, pf[nt], o[nt][dt]);
+        }
+    };
+
+#pragma unroll
+    for (int st = 0; st < C::NSTAGE - 1; ++st)
+        if (st < nstages) issue_stage(st);
+
+    for (int st = 0; st < nstages; ++st) {
+        // after the barrier every wave's pieces of stage st have landed and
+        // stage st-1 has been consumed, so its buffer can be refilled
+        if (st + 2 < nstages) stage_barrier<2 * C::DMA_PER_WAVE>();
+        else if (st + 1 < nstages) stage_barrier<C::DMA_PER_WAVE>();
+        else stage_barrier<0>();
+        if (st + C::NSTAGE - 1 < nstages) issue_stage(st + C::NSTAGE - 1);
+
+        const UnitInfo ui = unit_info(a, vi, upre, tab_start, tab_nlen, id.g, u0 + st);
+        // an own unit of stream f only concerns the rows of f
+        bool wave_has_rows = row_wave_active;
+        if (ui.stream >= 0) {
+            const int f0 = ui.stream * a.G, f1 = f0 + a.G;  // video rows of stream f
+            wave_has_rows = wave_has_rows && f0 < wrow0 + 16 * NT && f1 > wrow0;
+        }
+        const unsigned char* kbuf = lds + (st % C::NSTAGE) * C::STAGE;
+        const unsigned char* vbuf = kbuf + C::STAGE_K;
+        if (wave_has_rows) {
+            if (ui.stream < 0 && ui.nk == kUnit) {
+#pragma unroll
+                for (int b = 0; b < C::KW / 32; ++b) block(std::false_type{}, kbuf, vbuf, kg * C::KW + 32 * b, ui);
+            } else {
+#pragma unroll
+                for (int b = 0; b < C::KW / 32; ++b) {
+                    const int kb = kg * C::KW + 32 * b;
+                    if (kb < ui.nk) block(std::true_type{}, kbuf, vbuf, kb, ui);
+                }
+            }
+        }
+    }
+
+    // row normaliser: sum the 4 lane groups of each row
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) l_part[nt] = sum_over_groups(l_part[nt]);
+
+    if constexpr (WK == 2) {
+        // key group 1 hands its state to key group 0 through LDS
+        constexpr int OROW = D + 4;
+        constexpr int RW_ROWS = NT * 16;
+        float* obuf = reinterpret_cast<float*>(lds);
+        float* mbuf = obuf + WR * RW_ROWS * OROW;
+        float* lbuf = mbuf + WR * RW_ROWS;
+        __syncthreads();  // ring no longer read; every DMA has landed
+        if (kg == 1 && row_wave_active) {
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) {
+                const int r = rw * RW_ROWS + 16 * nt + l16;
+#pragma unroll
+                for (int dt = 0; dt < C::DT; ++dt)
+                    *reinterpret_cast<f32x4_t*>(obuf + r * OROW + 16 * dt + 4 * lg) = o[nt][dt];
                 if (lg == 0) {
-                    a.part_m[(long)it.slot * SEH + qr] = mall[nt];
-                    a.part_l[(long)it.slot * SEH + qr] = lall[nt];
+                    mbuf[r] = m_ref[nt];
+                    lbuf[r] = l_part[nt];
                 }
+            }
+        }
+        __syncthreads();
+        if (kg == 1) return;
+        if (row_wave_active) {
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) {
+                const int r = rw * RW_ROWS + 16 * nt + l16;
+                const float m1 = mbuf[r], l1 = lbuf[r];
+                const float M = fmaxf(m_ref[nt], m1);
+                const float f0 = fast_exp2(m_ref[nt] - M);
+                const float f1 = fast_exp2(m1 - M);
+                l_part[nt] = f0 * l_part[nt] + f1 * l1;
+                m_ref[nt] = M;
+#pragma unroll
+                for (int dt = 0; dt < C::DT; ++dt)
+                    o[nt][dt] = f0 * o[nt][dt] + f1 * *reinterpret_cast<const f32x4_t*>(obuf + r * OROW + 16 * dt + 4 * lg);
+            }
+        }
+    }
+
+    if (!row_wave_active) return;
+    const long SEH = (long)a.num_events * a.H_q;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+        const int r = 16 * (rw * NT + nt) + l16;
+        if (r < nrows) {
+            const long qr = row_qrow(a, vi, id.g, row0 + r);
+            float* dst = a.part_o + ((long)id.c * SEH + qr) * D;
+#pragma unroll
+            for (int dt = 0; dt < C::DT; ++dt) *reinterpret_cast<f32x4_t*>(dst + 16 * dt + 4 * lg) = o[nt][dt];
+            if (lg == 0) {
+                a.part_m[(long)id.c * SEH + qr] = m_ref[nt];
+                a.part_l[(long)id.c * SEH + qr] = l_part[nt];
             }
         }
     }

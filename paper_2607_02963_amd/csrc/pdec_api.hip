@@ -2,10 +2,12 @@
 // dispatch for the C ABI declared in include/pdec.h.
 //
 // A step is two launches on the caller's stream:
-//   1. the split pass — prefix items (video, kv head, chunk, row group) and
-//      tail items (stream, kv head, row group), each writing one partial
-//      softmax state per query row into the workspace;
-//   2. the merge — one wave per (stream, head) row, writing out and lse.
+//   1. the split pass — items (video, kv head, chunk, row group) over the
+//      virtual key sequence (prefix units, then each stream's own units),
+//      each writing one partial softmax state per query row into the
+//      workspace;
+//   2. the finish pass — per (stream, kv head): merge of the row's states,
+//      writing out and lse.
 // Nothing is allocated per call; the workspace is the caller's.
 #include <hip/hip_runtime.h>
 
@@ -18,7 +20,7 @@
 #include "pdec.h"
 
 #include "kernel_append.h"
-#include "kernel_merge.h"
+#include "kernel_finish.h"
 #include "kernel_mfma.h"
 #include "kernel_valu.h"
 
@@ -28,9 +30,8 @@ using namespace pdec;
 
 constexpr int kPathValu = 1;
 constexpr int kPathMfma = 2;
-constexpr int kTargetItems = 256;   // MI355X compute units: one item per CU per wave of items
-constexpr int kMfmaMaxTiles = 4;    // 16-row tiles per matrix-core item
-constexpr int kKeyAlign = 128;      // chunk lengths are whole 128-key blocks
+constexpr int kTargetItems = 256;   // MI355X compute units: one item per CU
+constexpr int kUnitKeys = kUnit;    // keys per unit of the virtual key sequence
 
 std::atomic<int> g_path_override{0};
 
@@ -43,43 +44,49 @@ long g_timer_calls = 0;
 struct Plan {
     int path;
     int rows_per_item;
-    int nt;            // row tiles per item (matrix-core path)
+    int shape;          // matrix-core work-group shape (1: 64, 2: 128, 3: 256 rows)
     int rg_max;
-    int tail_rg;
-    int chunk;
+    int unit_per_chunk;
     int max_chunks;
-    int slots;
-    long n_prefix_items;
-    long n_tail_items;
+    long n_items;
+    size_t part_floats; // floats of partial state
     size_t ws_bytes;
 };
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
 
+long ceil_div(long a, long b) { return (a + b - 1) / b; }
+
+int events_per_video(const pdec_dims* d)
+{
+    return d->max_events_per_video > 0 ? d->max_events_per_video : std::min(d->num_events, kMaxStreamsPerVideo);
+}
+
 int validate_dims(const pdec_dims* d, int num_videos)
 {
     if (!d) return PDEC_ERR_INVALID_ARG;
     if (num_videos < 1 || d->num_events < 1 || d->num_q_heads < 1 || d->num_kv_heads < 1 ||
         d->num_q_heads % d->num_kv_heads != 0 || d->event_cap < 1 || d->max_prefix_len < 0 ||
-        d->max_events_per_video < 0 || d->max_events_per_video > d->num_events)
+        d->max_events_per_video < 0 || d->max_events_per_video > d->num_events || d->prefix_tokens < 0)
         return PDEC_ERR_INVALID_ARG;
     if (d->dtype != PDEC_DTYPE_F32 && d->dtype != PDEC_DTYPE_BF16) return PDEC_ERR_UNSUPPORTED;
     if (d->head_dim != 64 && d->head_dim != 128) return PDEC_ERR_UNSUPPORTED;
     if (!(d->softmax_scale <= 0.f) && !std::isfinite(d->softmax_scale)) return PDEC_ERR_INVALID_ARG;
+    // one video's streams must fit the per-video unit table; a single-video
+    // call has all streams in one video
+    if (events_per_video(d) > kMaxStreamsPerVideo) return PDEC_ERR_UNSUPPORTED;
+    if (num_videos == 1 && d->num_events > kMaxStreamsPerVideo) return PDEC_ERR_UNSUPPORTED;
     // index arithmetic inside the kernels is 32-bit for row counts
-    const long rows = (long)d->num_events * d->num_q_heads;
-    if (rows > (1L << 30)) return PDEC_ERR_UNSUPPORTED;
+    if ((long)d->num_events * d->num_q_heads > (1L << 30)) return PDEC_ERR_UNSUPPORTED;
     return PDEC_OK;
 }
-
-int ceil_div(long a, long b) { return (int)((a + b - 1) / b); }
 
 Plan make_plan(const pdec_dims* d, int num_videos)
 {
     Plan p{};
     const int G = d->num_q_heads / d->num_kv_heads;
-    const int ev = d->max_events_per_video > 0 ? d->max_events_per_video : d->num_events;
+    const int ev = events_per_video(d);
     const long rows_max = (long)ev * G;  // query rows per (video, kv head)
     int path = (d->dtype == PDEC_DTYPE_BF16 && rows_max >= 16) ? kPathMfma : kPathValu;
     const int ov = g_path_override.load();
@@ -87,28 +94,34 @@ Plan make_plan(const pdec_dims* d, int num_videos)
     if (ov == kPathMfma && d->dtype == PDEC_DTYPE_BF16) path = kPathMfma;
     p.path = path;
     if (path == kPathMfma) {
-        const int tiles = ceil_div(rows_max, 16);
-        const int groups = ceil_div(tiles, kMfmaMaxTiles);
-        p.nt = ceil_div(tiles, groups);
-        p.rows_per_item = 16 * p.nt;
+        // 8 waves: up to 4 tiles -> 1 tile per row wave, 2 key groups (64 rows);
+        // up to 8 -> 2 tiles per row wave, 2 key groups (128 rows);
+        // more -> 2 tiles per row wave, 8 row waves (256 rows per item)
+        const long tiles = ceil_div(rows_max, 16);
+        p.shape = tiles <= 4 ? 1 : tiles <= 8 ? 2 : 3;
+        p.rows_per_item = tiles <= 4 ? 64 : tiles <= 8 ? 128 : 256;
     } else {
-        p.nt = 0;
+        p.shape = 0;
         p.rows_per_item = rows_max <= 8 ? 8 : 16;
     }
-    p.rg_max = ceil_div(rows_max, p.rows_per_item);
-    p.tail_rg = ceil_div(G, p.rows_per_item);
-    // chunk length: spread the prefix of the batch over about kTargetItems items
-    const long work = (long)std::max(d->max_prefix_len, 1) * num_videos * d->num_kv_heads * p.rg_max;
-    long chunk = (work + kTargetItems - 1) / kTargetItems;
-    chunk = (chunk + kKeyAlign - 1) / kKeyAlign * kKeyAlign;
-    chunk = std::max<long>(chunk, kKeyAlign);
-    p.chunk = (int)std::min<long>(chunk, 1L << 30);
-    p.max_chunks = std::max(1, ceil_div(d->max_prefix_len, p.chunk));
-    p.slots = p.max_chunks + 1;
-    p.n_prefix_items = (long)num_videos * d->num_kv_heads * p.max_chunks * p.rg_max;
-    p.n_tail_items = (long)d->num_events * d->num_kv_heads * p.tail_rg;
+    p.rg_max = (int)ceil_div(rows_max, p.rows_per_item);
+    // Units of the virtual key sequence of one (video, kv head): prefix units
+    // plus each stream's own units.  The chunk length aims at about one item
+    // per compute unit for a batch whose streams hold about one unit each;
+    // the slot count covers the worst case (every cache full).
+    const long own_units_max = (long)ev * ceil_div(d->event_cap, kUnitKeys);
+    const long units_max = ceil_div(d->max_prefix_len, kUnitKeys) + own_units_max;
+    const long tokens = d->prefix_tokens > 0 ? d->prefix_tokens : (long)num_videos * d->max_prefix_len;
+    const long units_expected = ceil_div(tokens, kUnitKeys) + (long)d->num_events;
+    long upc = ceil_div(units_expected * d->num_kv_heads * p.rg_max, kTargetItems);
+    upc = std::max<long>(upc, ceil_div(std::max<long>(units_max, 1), kMaxChunks));
+    upc = std::max<long>(upc, 1);
+    p.unit_per_chunk = (int)std::min<long>(upc, 1L << 24);
+    p.max_chunks = (int)std::max<long>(1, ceil_div(units_max, p.unit_per_chunk));
+    p.n_items = (long)num_videos * d->num_kv_heads * p.max_chunks * p.rg_max;
     const size_t rows = (size_t)d->num_events * d->num_q_heads;
-    p.ws_bytes = (size_t)p.slots * rows * ((size_t)d->head_dim + 2) * sizeof(float);
+    p.part_floats = (size_t)p.max_chunks * rows * ((size_t)d->head_dim + 2);
+    p.ws_bytes = p.part_floats * sizeof(float) + (size_t)num_videos * sizeof(int32_t);
     return p;
 }
 
@@ -118,20 +131,13 @@ int launch_status()
     return e == hipSuccess ? PDEC_OK : PDEC_ERR_HIP;
 }
 
-template <int D, int NT>
-void launch_mfma_nt(const StepArgs& a, int grid, hipStream_t s)
-{
-    hipLaunchKernelGGL((split_mfma_kernel<D, NT>), dim3(grid), dim3(256), 0, s, a);
-}
-
 template <int D>
-void launch_mfma(const StepArgs& a, int nt, int grid, hipStream_t s)
+void launch_mfma(const StepArgs& a, int shape, int grid, hipStream_t s)
 {
-    switch (nt) {
-    case 1: launch_mfma_nt<D, 1>(a, grid, s); break;
-    case 2: launch_mfma_nt<D, 2>(a, grid, s); break;
-    case 3: launch_mfma_nt<D, 3>(a, grid, s); break;
-    default: launch_mfma_nt<D, 4>(a, grid, s); break;
+    switch (shape) {
+    case 1: hipLaunchKernelGGL((split_mfma_kernel<D, 1, 4, 2>), dim3(grid), dim3(512), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((split_mfma_kernel<D, 2, 4, 2>), dim3(grid), dim3(512), 0, s, a); break;
+    default: hipLaunchKernelGGL((split_mfma_kernel<D, 2, 8, 1>), dim3(grid), dim3(512), 0, s, a); break;
     }
 }
 
@@ -164,7 +170,7 @@ int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_pr
     }
     const Plan p = make_plan(d, num_videos);
     if (workspace_bytes < p.ws_bytes) return PDEC_ERR_WORKSPACE;
-    if (p.n_prefix_items + p.n_tail_items > (long)INT32_MAX) return PDEC_ERR_UNSUPPORTED;
+    if (8 * ceil_div(p.n_items, 8) > (long)INT32_MAX) return PDEC_ERR_UNSUPPORTED;
 
     StepArgs a{};
     a.q = q;
@@ -180,8 +186,9 @@ int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_pr
     a.lse = lse;
     const size_t rows = (size_t)d->num_events * d->num_q_heads;
     a.part_o = static_cast<float*>(workspace);
-    a.part_m = a.part_o + (size_t)p.slots * rows * d->head_dim;
-    a.part_l = a.part_m + (size_t)p.slots * rows;
+    a.part_m = a.part_o + (size_t)p.max_chunks * rows * d->head_dim;
+    a.part_l = a.part_m + (size_t)p.max_chunks * rows;
+    a.video_chunks = reinterpret_cast<int32_t*>(a.part_o + p.part_floats);
     a.num_videos = num_videos;
     a.num_events = d->num_events;
     a.H_q = d->num_q_heads;
@@ -189,25 +196,25 @@ int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_pr
     a.D = d->head_dim;
     a.cap = d->event_cap;
     a.G = d->num_q_heads / d->num_kv_heads;
-    a.chunk = p.chunk;
+    a.unit_per_chunk = p.unit_per_chunk;
     a.max_chunks = p.max_chunks;
     a.rows_per_item = p.rows_per_item;
     a.rg_max = p.rg_max;
-    a.tail_rg = p.tail_rg;
-    a.n_prefix_items = (int)p.n_prefix_items;
-    a.n_tail_items = (int)p.n_tail_items;
+    a.n_items = (int)p.n_items;
+    // blocks: every chunk of every XCD round (see item_of_block) times the row groups
+    a.items_per_xcd = (int)(p.rg_max * ceil_div(p.n_items / p.rg_max, 8));
     const float scale = d->softmax_scale > 0.f ? d->softmax_scale : 1.f / std::sqrt((float)d->head_dim);
     a.qscale = scale * 1.4426950408889634f;
 
     hipStream_t s = static_cast<hipStream_t>(stream);
-    const int grid = (int)(p.n_prefix_items + p.n_tail_items);
+    const int grid = 8 * a.items_per_xcd;
     const bool bf16 = d->dtype == PDEC_DTYPE_BF16;
     const int timer_slot = g_timer_n > 0 ? (int)(g_timer_calls++ % g_timer_n) : -1;
     if (timer_slot >= 0 && hipEventRecord(static_cast<hipEvent_t>(g_timer_start[timer_slot]), s) != hipSuccess)
         return PDEC_ERR_HIP;
     if (p.path == kPathMfma) {
-        if (d->head_dim == 128) launch_mfma<128>(a, p.nt, grid, s);
-        else launch_mfma<64>(a, p.nt, grid, s);
+        if (d->head_dim == 128) launch_mfma<128>(a, p.shape, grid, s);
+        else launch_mfma<64>(a, p.shape, grid, s);
     } else if (bf16) {
         if (d->head_dim == 128) launch_valu<uint16_t, 128>(a, p.rows_per_item, grid, s);
         else launch_valu<uint16_t, 64>(a, p.rows_per_item, grid, s);
@@ -218,13 +225,13 @@ int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_pr
     if ((rc = launch_status()) != PDEC_OK) return rc;
     if (timer_slot >= 0 && hipEventRecord(static_cast<hipEvent_t>(g_timer_stop[timer_slot]), s) != hipSuccess)
         return PDEC_ERR_HIP;
-    const int mgrid = (int)rows;
+    const int fgrid = d->num_events * d->num_kv_heads;
     if (bf16) {
-        if (d->head_dim == 128) hipLaunchKernelGGL((merge_kernel<uint16_t, 128>), dim3(mgrid), dim3(64), 0, s, a);
-        else hipLaunchKernelGGL((merge_kernel<uint16_t, 64>), dim3(mgrid), dim3(64), 0, s, a);
+        if (d->head_dim == 128) hipLaunchKernelGGL((finish_kernel<uint16_t, 128>), dim3(fgrid), dim3(1024), 0, s, a);
+        else hipLaunchKernelGGL((finish_kernel<uint16_t, 64>), dim3(fgrid), dim3(1024), 0, s, a);
     } else {
-        if (d->head_dim == 128) hipLaunchKernelGGL((merge_kernel<float, 128>), dim3(mgrid), dim3(64), 0, s, a);
-        else hipLaunchKernelGGL((merge_kernel<float, 64>), dim3(mgrid), dim3(64), 0, s, a);
+        if (d->head_dim == 128) hipLaunchKernelGGL((finish_kernel<float, 128>), dim3(fgrid), dim3(1024), 0, s, a);
+        else hipLaunchKernelGGL((finish_kernel<float, 64>), dim3(fgrid), dim3(1024), 0, s, a);
     }
     return launch_status();
 }
@@ -321,7 +328,7 @@ int pdec_query_plan(const pdec_dims* dims, int32_t num_videos, int32_t* path, in
     if (rc != PDEC_OK) return rc;
     const Plan p = make_plan(dims, num_videos);
     if (path) *path = p.path;
-    if (chunk_keys) *chunk_keys = p.chunk;
+    if (chunk_keys) *chunk_keys = p.unit_per_chunk * kUnitKeys;
     return PDEC_OK;
 }
 

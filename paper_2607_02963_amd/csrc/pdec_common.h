@@ -1,20 +1,22 @@
 // Device-side definitions shared by the pdec kernels (gfx950).
 //
-// Work decomposition of one decode step (§3.4, Eq. 3: every stream's query
-// reads the whole shared prefix plus its own rows):
+// Work decomposition of one decode step (§3.4, Eq. 3).  For one video and
+// one kv head g, the query rows are r = stream_local * G + j (stream e of the
+// video, query head g*G + j).  A row of stream f sees every prefix key and
+// the n_f rows of f's own cache, nothing else.  The split pass walks, per
+// (video, kv head), a virtual key sequence cut into 64-key units:
 //
-//   * prefix items  (video v, kv head g, chunk c, row group rg): the query rows
-//     of video v that read kv head g, i.e. rows r = (stream, head) with
-//     stream in v and head in g's group, ordered r = stream_local * G + j,
-//     take chunk c (keys [c*chunk, (c+1)*chunk) of v's prefix) and produce a
-//     partial softmax state (running max m, normaliser l, un-normalised
-//     output o) into slot c.  The prefix K/V tile is read from HBM once for
-//     all of its rows — the point of decoding the streams together.
-//   * tail items    (stream e, kv head g, row group): the G query rows of
-//     stream e that read kv head g, over the n_e own rows of e's cache, into
-//     the last slot.  Rows of other streams are never addressed (the mask).
-//   * merge         per (stream, head): combines the slots of that row with
-//     the log-sum-exp rule and writes out / lse.
+//   [ prefix units: ceil(L/64) ] [ stream 0 own units ] [ stream 1 ... ] ...
+//
+// stream f contributing ceil(n_f/64) units (none once it has ended).  A
+// prefix unit is read by every row; an own unit of stream f only by the
+// rows of f (other rows are masked).  Units are dealt to chunks of
+// `unit_per_chunk`; a work item (video, kv head, chunk, row group) runs its
+// units and leaves one partial softmax state (max m, normaliser l,
+// un-normalised output o) per row in slot `chunk`.  Each prefix K/V byte is
+// fetched once for all rows of the item — the point of decoding the streams
+// together — and a stream's own rows are fetched once for its G rows.
+// The finish pass merges the slots of each row.
 //
 // Scores are kept in base-2 units: q is pre-multiplied by scale*log2(e), so
 // exp2 replaces exp and lse = ln(2) * (m + log2 l).
@@ -27,6 +29,8 @@ namespace pdec {
 
 constexpr float kNegInf = -__builtin_inff();
 constexpr float kLn2 = 0.69314718055994530942f;
+constexpr int kUnit = 64;                 // keys per unit of the virtual key sequence
+constexpr int kMaxStreamsPerVideo = 2048; // size of the per-video unit table in LDS
 
 // Everything a step kernel needs; passed by value.
 struct StepArgs {
@@ -41,19 +45,19 @@ struct StepArgs {
     const int32_t* prefix_len;  // one video: [1]; null for a ragged batch
     void* out;
     float* lse;                 // may be null
-    float* part_o;              // [slots, SE*H_q, D]
-    float* part_m;              // [slots, SE*H_q]
-    float* part_l;              // [slots, SE*H_q]
+    float* part_o;              // [max_chunks, SE*H_q, D]
+    float* part_m;              // [max_chunks, SE*H_q]
+    float* part_l;              // [max_chunks, SE*H_q]
+    int32_t* video_chunks;      // [V]: chunks holding states, written by the split pass
     int num_videos;
     int num_events;             // SE
     int H_q, H_kv, D, cap, G;
-    int chunk;                  // keys per prefix chunk
-    int max_chunks;             // chunk slots; slot max_chunks holds the tail
-    int rows_per_item;          // query rows per work item (RT)
+    int unit_per_chunk;         // units per chunk
+    int max_chunks;             // chunk slots per video
+    int rows_per_item;          // query rows per work item
     int rg_max;                 // row groups per (video, kv head, chunk)
-    int tail_rg;                // row groups per (stream, kv head)
-    int n_prefix_items;
-    int n_tail_items;
+    int n_items;
+    int items_per_xcd;          // ceil(n_items / 8)
     float qscale;               // softmax scale * log2(e)
 };
 
@@ -90,73 +94,99 @@ __device__ inline int video_of_event(const StepArgs& a, int e)
     return lo;
 }
 
-// One work item of the split pass: a run of keys (row stride key_stride
-// elements) against a set of query rows.
-struct Item {
-    long key_off;    // element offset of the first key (K and V share layout)
-    bool prefix;     // keys come from the prefix (else from a stream cache)
-    int nkeys;
-    int ebase;       // first stream of the row numbering
-    int row0;        // first row of this item in that numbering
-    int nrows;       // rows in this item (<= rows_per_item)
-    int g;           // kv head
-    int slot;        // partial slot written
-};
-
-__device__ inline bool decode_item(const StepArgs& a, int b, Item& it)
+// Work item of hardware block b.  Blocks are dispatched round-robin over the
+// 8 XCDs (block b runs on XCD b % 8), each XCD with its own L2.  Chunks are
+// dealt round-robin over the XCDs, so chunk slots a video does not fill are
+// spread evenly and no XCD gets more busy items than its share; the row
+// groups of one chunk, which read the same keys, go to the same XCD one
+// after another.  With a single row group this is the identity.  Returns -1
+// for blocks past the last item.
+__device__ inline int item_of_block(const StepArgs& a, int b)
 {
-    const int RT = a.rows_per_item;
-    if (b < a.n_prefix_items) {
-        const int rg = b % a.rg_max;
-        b /= a.rg_max;
-        const int c = b % a.max_chunks;
-        b /= a.max_chunks;
-        const int g = b % a.H_kv;
-        const int v = b / a.H_kv;
-        const VideoInfo vi = video_info(a, v);
-        const int k0 = c * a.chunk;
-        if (k0 >= vi.L) return false;
-        const int R = vi.E * a.G;
-        const int row0 = rg * RT;
-        if (row0 >= R) return false;
-        it.prefix = true;
-        it.nkeys = min(a.chunk, vi.L - k0);
-        it.key_off = ((long)(vi.p0 + k0) * a.H_kv + g) * a.D;
-        it.ebase = vi.e0;
-        it.row0 = row0;
-        it.nrows = min(RT, R - row0);
-        it.g = g;
-        it.slot = c;
-        return true;
-    }
-    b -= a.n_prefix_items;
-    if (b >= a.n_tail_items) return false;
-    const int rg = b % a.tail_rg;
-    b /= a.tail_rg;
-    const int g = b % a.H_kv;
-    const int e = b / a.H_kv;
-    const int n = a.event_lens[e];
-    if (n <= 0) return false;
-    const int row0 = rg * RT;
-    if (row0 >= a.G) return false;
-    it.prefix = false;
-    it.nkeys = n;
-    it.key_off = ((long)e * a.cap * a.H_kv + g) * a.D;
-    it.ebase = e;
-    it.row0 = row0;
-    it.nrows = min(RT, a.G - row0);
-    it.g = g;
-    it.slot = a.max_chunks;
-    return true;
+    const int x = b % 8, j = b / 8;
+    const int item = ((j / a.rg_max) * 8 + x) * a.rg_max + j % a.rg_max;
+    return item < a.n_items ? item : -1;
 }
 
-// Global (stream, head) row index of row r of an item.
-__device__ inline int item_qrow(const StepArgs& a, const Item& it, int r)
+struct ItemId {
+    int v, g, c, rg;
+};
+
+__device__ inline ItemId item_id(const StepArgs& a, int item)
 {
-    const int rr = it.row0 + r;
-    const int stream = it.ebase + rr / a.G;
-    const int head = it.g * a.G + rr % a.G;
-    return stream * a.H_q + head;
+    ItemId id;
+    id.rg = item % a.rg_max;
+    item /= a.rg_max;
+    id.c = item % a.max_chunks;
+    item /= a.max_chunks;
+    id.g = item % a.H_kv;
+    id.v = item / a.H_kv;
+    return id;
+}
+
+// Per-video unit table, built in LDS by wave 0 of a work-group:
+//   start[f] = first own unit of stream f (relative to the first own unit),
+//   nlen[f]  = n_f (<= 0 stored as 0); start[E] = total own units.
+// Streams that have ended contribute no units.  Returns the total.
+__device__ inline int build_unit_table(const StepArgs& a, const VideoInfo& vi, int* start, int* nlen)
+{
+    const int lane = threadIdx.x & 63;
+    int base = 0;
+    for (int f0 = 0; f0 < vi.E; f0 += 64) {
+        const int f = f0 + lane;
+        const int n = f < vi.E ? max(a.event_lens[vi.e0 + f], 0) : 0;
+        const int units = (n + kUnit - 1) / kUnit;
+        int incl = units;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int y = __shfl_up(incl, off);
+            if (lane >= off) incl += y;
+        }
+        if (f < vi.E) {
+            start[f] = base + incl - units;
+            nlen[f] = n;
+        }
+        base += __shfl(incl, 63);
+    }
+    if (lane == 0) start[vi.E] = base;
+    return base;
+}
+
+// What one unit of the virtual key sequence is.
+struct UnitInfo {
+    long key_off;  // element offset of its first key in k/v_prefix or k/v_event
+    int nk;        // valid keys (1..64)
+    int stream;    // -1 for a prefix unit, else the video-local stream whose rows see it
+};
+
+__device__ inline UnitInfo unit_info(const StepArgs& a, const VideoInfo& vi, int upre, const int* start,
+                                     const int* nlen, int g, int u)
+{
+    UnitInfo ui;
+    if (u < upre) {
+        const int k0 = u * kUnit;
+        ui.key_off = ((long)(vi.p0 + k0) * a.H_kv + g) * a.D;
+        ui.nk = min(kUnit, vi.L - k0);
+        ui.stream = -1;
+        return ui;
+    }
+    const int uo = u - upre;
+    int lo = 0, hi = vi.E - 1;  // last stream with start <= uo
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (start[mid] <= uo) lo = mid; else hi = mid - 1;
+    }
+    const int t0 = (uo - start[lo]) * kUnit;
+    ui.key_off = (((long)(vi.e0 + lo) * a.cap + t0) * a.H_kv + g) * a.D;
+    ui.nk = min(kUnit, nlen[lo] - t0);
+    ui.stream = lo;
+    return ui;
+}
+
+// Global (stream, head) row of item row r (r counted from 0 within the video).
+__device__ inline int row_qrow(const StepArgs& a, const VideoInfo& vi, int g, int r)
+{
+    return (vi.e0 + r / a.G) * a.H_q + g * a.G + r % a.G;
 }
 
 // Element conversions.  bf16 travels as its 16-bit pattern.
@@ -175,5 +205,9 @@ template <> __device__ inline uint16_t from_f32<uint16_t>(float x)
 }
 
 __device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// LDS-only barrier: waits for this wave's LDS operations, not its global
+// loads (a plain __syncthreads() also drains every outstanding global load).
+__device__ inline void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 }  // namespace pdec

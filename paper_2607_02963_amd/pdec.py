@@ -36,7 +36,7 @@ class Dims(ctypes.Structure):
                 ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("event_cap", ctypes.c_int32), ("max_prefix_len", ctypes.c_int32),
                 ("max_events_per_video", ctypes.c_int32), ("dtype", ctypes.c_int32),
-                ("softmax_scale", ctypes.c_float)]
+                ("softmax_scale", ctypes.c_float), ("prefix_tokens", ctypes.c_int64)]
 
 
 class PdecError(RuntimeError):
@@ -119,9 +119,9 @@ def _stream(stream, device) -> ctypes.c_void_p:
 
 
 def make_dims(num_events, H_q, H_kv, D, cap, max_prefix_len, dtype_code, scale=0.0,
-              max_events_per_video=0) -> Dims:
+              max_events_per_video=0, prefix_tokens=0) -> Dims:
     return Dims(int(num_events), int(H_q), int(H_kv), int(D), int(cap), int(max_prefix_len),
-                int(max_events_per_video), int(dtype_code), float(scale))
+                int(max_events_per_video), int(dtype_code), float(scale), int(prefix_tokens))
 
 
 def workspace_size(dims: Dims, num_videos: int = 1) -> int:
@@ -199,7 +199,8 @@ def attn_step_ragged(q, k_prefix, v_prefix, cu_prefix, k_event, v_event, event_l
     H_kv = k_prefix.shape[1]
     cap = k_event.shape[1]
     V = cu_prefix.shape[0] - 1
-    dims = make_dims(SE, H_q, H_kv, D, cap, max_prefix_len, _dtype_code(q), scale, max_events_per_video)
+    dims = make_dims(SE, H_q, H_kv, D, cap, max_prefix_len, _dtype_code(q), scale, max_events_per_video,
+                     prefix_tokens=k_prefix.shape[0])
     ws_bytes = workspace_size(dims, V)
     out, lse, workspace = _outputs(q, out, lse, workspace, ws_bytes)
     if cu_events.shape[0] != V + 1 or k_event.shape[0] != SE or event_lens.shape[0] != SE:

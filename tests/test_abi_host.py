@@ -48,11 +48,14 @@ def test_workspace_size_rejects_bad_dims():
 
 
 def test_workspace_holds_every_partial_slot():
+    """Slots cover the worst case: every prefix unit plus every stream's cache
+    full (129 rows -> 3 units of 64 keys), cut into chunks of chunk_keys."""
     d = _dims()
     path, chunk = pdec.query_plan(d)
-    slots = -(-32768 // chunk) + 1
-    assert pdec.workspace_size(d) == slots * 32 * 28 * (128 + 2) * 4
-    assert chunk % 128 == 0
+    assert chunk % 64 == 0
+    units_max = 32768 // 64 + 32 * 3
+    slots = -(-units_max // (chunk // 64))
+    assert pdec.workspace_size(d) == slots * 32 * 28 * (128 + 2) * 4 + 4
 
 
 @pytest.mark.parametrize("E,G,dt,expect", [(32, 7, pdec.PDEC_DTYPE_BF16, pdec.PATH_MFMA),
