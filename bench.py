@@ -68,6 +68,27 @@ def split_kernel_bytes(s) -> int:
     return 2 * int(s.cu_prefix[-1]) * row + 2 * int(s.event_lens.sum()) * row + s.num_events * s.H_q * s.D * b
 
 
+PROFILE = os.path.join(ROOT, "profiles", "split_finish__long_L32768_E32__hbm_counters.txt")
+
+
+def measured_traffic(workload_name: str):
+    """HBM bytes per split-kernel launch from the stored FETCH_SIZE/WRITE_SIZE
+    counters, scaled by the copy-kernel calibration; None unless they were
+    taken on this workload with the kernels as built now."""
+    from paper_2607_02963_amd import _build
+    if workload_name != "long_L32768_E32" or not os.path.exists(PROFILE):
+        return None
+    fields = {}
+    with open(PROFILE) as fh:
+        for line in fh:
+            if not line.startswith("#") and ":" in line:
+                k, v = line.split(":", 1)
+                fields[k.strip()] = v.strip()
+    if fields.get("source_digest") != _build.source_digest():
+        return None
+    return int(fields["traffic_bytes_per_launch"])
+
+
 def cpu_baseline(s):
     """The oracle (as it stands) on the host cores: one full step, all rows."""
     sys.path.insert(0, os.path.join(ROOT, "oracle"))
@@ -191,7 +212,7 @@ def main():
         "algorithmic_bytes_per_step": alg,
         "tokens_per_s": round(live / (ms * 1e-3), 1),
         "roofline": {"bound": "hbm", "achieved": round(kgbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(kgbps / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "frac": round(kgbps / HBM_PEAK_GBPS, 4), "traffic": measured_traffic(s.name),
                      "kernel": "split pass (shared prefix + stream rows)", "kernel_us": round(split_ms * 1e3, 3),
                      "kernel_algorithmic_bytes": kbytes},
     }

@@ -1,6 +1,7 @@
 """Builds libpdec.so (the HIP kernels and the C ABI) in-tree for gfx950."""
 from __future__ import annotations
 
+import hashlib
 import os
 import subprocess
 
@@ -19,6 +20,19 @@ HIP_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
 
 def sources():
     return [os.path.join(CSRC, f) for f in sorted(os.listdir(CSRC)) if f.endswith(".hip")]
+
+
+def source_digest() -> str:
+    """sha256 over the kernel sources, the public header and the compile
+    flags: names the build a stored profile was measured with."""
+    h = hashlib.sha256()
+    for d in (CSRC, INCLUDE):
+        for f in sorted(os.listdir(d)):
+            h.update(f.encode())
+            with open(os.path.join(d, f), "rb") as fh:
+                h.update(fh.read())
+    h.update(" ".join(HIP_FLAGS).encode())
+    return h.hexdigest()
 
 
 def build_library(verbose: bool = False, extra_flags=()) -> str:

@@ -10,11 +10,12 @@
 // far below any score, so its weight is 0.
 // A stream with n_e == 0 has ended: out row 0, lse -inf.
 //
-// One work-group of 1024 lanes per (stream e, kv head g).  Per pass of up to
-// RP rows: a wave per row reduces (M, L) over the slots and stores each
-// slot's weight 2^(m_c - M) in LDS; then four lane groups each take every
-// fourth slot, 4 d per lane, so every load of the pass is in flight at once,
-// and their sums meet in LDS.
+// One work-group of four waves per row.  A row's slots are contiguous in the
+// workspace ([row][slot][D] and [row][slot](m, l)).  The lanes form 4*SG
+// slot groups of D/4 lanes (4 d each); group s takes slots s, s + 4SG, ...
+// Their first NL slots are loaded before anything else, so those loads are
+// in flight while wave 0 reduces (M, L) and stores the slot weights
+// 2^(m_c - M) in LDS; the group sums then meet through lane shuffles and LDS.
 #pragma once
 
 #include "pdec_common.h"
@@ -24,92 +25,109 @@ namespace pdec {
 constexpr int kMaxChunks = 512;  // slot weights held in LDS per row
 
 template <typename T, int D>
-__global__ __launch_bounds__(1024) void finish_kernel(StepArgs a)
+__global__ __launch_bounds__(256) void finish_kernel(StepArgs a)
 {
-    constexpr int NT = 1024, SG = 4, GT = NT / SG;  // slot groups, lanes per group
-    constexpr int TPR = D / 4;                      // lanes per row (4 d each)
-    constexpr int RP = GT / TPR;                    // rows per pass
-    __shared__ float wts[RP][kMaxChunks];
-    __shared__ float4 red[SG - 1][GT];
-    __shared__ float M_s[RP], L_s[RP];
+    constexpr int NW = 4;             // waves per row
+    constexpr int TPR = D / 4;        // lanes per slot group
+    constexpr int SG = 64 / TPR;      // slot groups per wave
+    constexpr int GS = NW * SG;       // slot groups per row
+    constexpr int NL = 64 / GS;       // slots per group loaded up front (64 slots in all)
+    static_assert(SG * TPR == 64, "head_dim 64 or 128");
+    __shared__ float wts[kMaxChunks];
+    __shared__ float4 red[NW][TPR];
+    __shared__ float ML_s[2];
 
-    const int e = blockIdx.x / a.H_kv;
-    const int g = blockIdx.x % a.H_kv;
     const int tid = threadIdx.x;
-    const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int sg = tid / GT;
-    const int t = tid % GT;
-    const int row = t / TPR;
-    const int d0 = 4 * (t % TPR);
-    const long SEH = (long)a.num_events * a.H_q;
-    const long qrow0 = (long)e * a.H_q + (long)g * a.G;  // first (stream, head) row of the group
-    T* __restrict__ out = static_cast<T*>(a.out);
+    const int lane = tid & 63;
+    const long qr = blockIdx.x;  // (stream, head) row
+    const int e = (int)(qr / a.H_q);
+    T* __restrict__ out = static_cast<T*>(a.out) + qr * D;
 
-    if (a.event_lens[e] <= 0) {  // ended stream: the whole work-group takes this branch
-        for (int i = tid; i < a.G * D; i += NT) out[qrow0 * D + i] = from_f32<T>(0.f);
-        if (a.lse && tid < a.G) a.lse[qrow0 + tid] = kNegInf;
+    if (a.event_lens[e] <= 0) {  // ended stream: uniform over the work-group
+        if (tid < D) out[tid] = from_f32<T>(0.f);
+        if (a.lse && tid == 0) a.lse[qr] = kNegInf;
         return;
     }
     const int nch = min(a.video_chunks[video_of_event(a, e)], a.max_chunks);
+    const int grp = wave * SG + lane / TPR;
+    const int d0 = 4 * (lane % TPR);
+    const float* __restrict__ po = a.part_o + qr * a.max_chunks * D + d0;
 
-    for (int r0 = 0; r0 < a.G; r0 += RP) {
-        const int nrows = min(RP, a.G - r0);
-        for (int r = wave; r < nrows; r += NT / 64) {
-            const long qr = qrow0 + r0 + r;
-            float mx = kNegInf;
-            for (int c = lane; c < nch; c += 64) mx = fmaxf(mx, a.part_m[c * SEH + qr]);
+    float4 x[NL];
 #pragma unroll
-            for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
-            float ls = 0.f;
-            for (int c = lane; c < nch; c += 64) {
-                const float w = fast_exp2(a.part_m[c * SEH + qr] - mx);  // 0 for an empty slot
-                wts[r][c] = w;
-                ls += w * a.part_l[c * SEH + qr];
-            }
+    for (int i = 0; i < NL; ++i) {
+        const int c = grp + GS * i;
+        x[i] = c < nch ? *reinterpret_cast<const float4*>(po + (long)c * D) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+
+    if (wave == 0) {
+        const float2* __restrict__ ml = reinterpret_cast<const float2*>(a.part_ml) + qr * a.max_chunks;
+        float mx = kNegInf;
+        for (int c = lane; c < nch; c += 64) mx = fmaxf(mx, ml[c].x);
 #pragma unroll
-            for (int off = 32; off > 0; off >>= 1) ls += __shfl_xor(ls, off);
-            if (lane == 0) {
-                M_s[r] = mx;
-                L_s[r] = ls;
-            }
+        for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+        float ls = 0.f;
+        for (int c = lane; c < nch; c += 64) {
+            const float2 s = ml[c];
+            const float w = fast_exp2(s.x - mx);  // 0 for a slot without keys of this row
+            wts[c] = w;
+            ls += w * s.y;
         }
-        __syncthreads();
-        float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (row < nrows) {
-            const long qr = qrow0 + r0 + row;
-            const float* po = a.part_o + qr * D + d0;
-#pragma unroll 16
-            for (int c = sg; c < nch; c += SG) {
-                const float w = wts[row][c];
-                const float4 x = *reinterpret_cast<const float4*>(po + c * SEH * D);
-                acc.x += w * x.x;
-                acc.y += w * x.y;
-                acc.z += w * x.z;
-                acc.w += w * x.w;
-            }
-        }
-        if (sg > 0) red[sg - 1][t] = acc;
-        __syncthreads();
-        if (sg == 0 && row < nrows) {
 #pragma unroll
-            for (int j = 0; j < SG - 1; ++j) {
-                const float4 y = red[j][t];
-                acc.x += y.x;
-                acc.y += y.y;
-                acc.z += y.z;
-                acc.w += y.w;
-            }
-            const long qr = qrow0 + r0 + row;
-            const float inv = 1.f / L_s[row];
-            T* dst = out + qr * D + d0;
-            dst[0] = from_f32<T>(acc.x * inv);
-            dst[1] = from_f32<T>(acc.y * inv);
-            dst[2] = from_f32<T>(acc.z * inv);
-            dst[3] = from_f32<T>(acc.w * inv);
-            if (a.lse && d0 == 0) a.lse[qr] = kLn2 * (M_s[row] + __log2f(L_s[row]));
+        for (int off = 32; off > 0; off >>= 1) ls += __shfl_xor(ls, off);
+        if (lane == 0) {
+            ML_s[0] = mx;
+            ML_s[1] = ls;
         }
-        __syncthreads();  // LDS reused by the next pass
+    }
+    __syncthreads();
+
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int i = 0; i < NL; ++i) {
+        const int c = grp + GS * i;
+        if (c < nch) {
+            const float w = wts[c];
+            acc.x += w * x[i].x;
+            acc.y += w * x[i].y;
+            acc.z += w * x[i].z;
+            acc.w += w * x[i].w;
+        }
+    }
+    for (int c = grp + GS * NL; c < nch; c += GS) {  // rows with more than 64 slots
+        const float w = wts[c];
+        const float4 y = *reinterpret_cast<const float4*>(po + (long)c * D);
+        acc.x += w * y.x;
+        acc.y += w * y.y;
+        acc.z += w * y.z;
+        acc.w += w * y.w;
+    }
+#pragma unroll
+    for (int off = TPR; off < 64; off <<= 1) {
+        acc.x += __shfl_xor(acc.x, off);
+        acc.y += __shfl_xor(acc.y, off);
+        acc.z += __shfl_xor(acc.z, off);
+        acc.w += __shfl_xor(acc.w, off);
+    }
+    if (lane < TPR) red[wave][lane] = acc;
+    __syncthreads();
+    if (wave == 0 && lane < TPR) {
+#pragma unroll
+        for (int w = 1; w < NW; ++w) {
+            const float4 y = red[w][lane];
+            acc.x += y.x;
+            acc.y += y.y;
+            acc.z += y.z;
+            acc.w += y.w;
+        }
+        const float mx = ML_s[0], ls = ML_s[1];
+        const float inv = 1.f / ls;
+        out[d0] = from_f32<T>(acc.x * inv);
+        out[d0 + 1] = from_f32<T>(acc.y * inv);
+        out[d0 + 2] = from_f32<T>(acc.z * inv);
+        out[d0 + 3] = from_f32<T>(acc.w * inv);
+        if (a.lse && lane == 0) a.lse[qr] = kLn2 * (mx + __log2f(ls));
     }
 }
 

@@ -57,10 +57,13 @@ __device__ inline f32x4_t mfma_16x16x32(bf16x8_t a, bf16x8_t b, f32x4_t c)
 
 __device__ inline bf16x8_t as_bf16x8(u32x4_t x) { return __builtin_bit_cast(bf16x8_t, x); }
 
+typedef __attribute__((ext_vector_type(2))) float f32x2_t;
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
+
+// Two floats to a bf16 pair (round to nearest even), one v_cvt_pk_bf16_f32.
 __device__ inline uint32_t pack_bf16x2(float lo, float hi)
 {
-    const __bf16 a = static_cast<__bf16>(lo), b = static_cast<__bf16>(hi);
-    return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));
 }
 
 // Reductions over the 4 lane groups (lanes l, l^16, l^32, l^48) that hold one
@@ -436,19 +439,16 @@ __global__ __launch_bounds__(512) void split_mfma_kernel(StepArgs a)
     }
 
     if (!row_wave_active) return;
-    const long SEH = (long)a.num_events * a.H_q;
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
         const int r = 16 * (rw * NT + nt) + l16;
         if (r < nrows) {
             const long qr = row_qrow(a, vi, id.g, row0 + r);
-            float* dst = a.part_o + ((long)id.c * SEH + qr) * D;
+            const long slot = qr * a.max_chunks + id.c;
+            float* dst = a.part_o + slot * D;
 #pragma unroll
             for (int dt = 0; dt < C::DT; ++dt) *reinterpret_cast<f32x4_t*>(dst + 16 * dt + 4 * lg) = o[nt][dt];
-            if (lg == 0) {
-                a.part_m[(long)id.c * SEH + qr] = m_ref[nt];
-                a.part_l[(long)id.c * SEH + qr] = l_part[nt];
-            }
+            if (lg == 0) *reinterpret_cast<float2*>(a.part_ml + 2 * slot) = make_float2(m_ref[nt], l_part[nt]);
         }
     }
 }

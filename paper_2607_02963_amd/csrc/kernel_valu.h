@@ -177,16 +177,15 @@ __global__ __launch_bounds__(256) void split_valu_kernel(StepArgs a)
         }
     }
 
-    const long SEH = (long)a.num_events * a.H_q;
 #pragma unroll
     for (int i = 0; i < OPT; ++i) {
         const int idx = tid + NT * i;
         const int r = idx / D, d = idx % D;
-        if (r < nrows) a.part_o[((long)id.c * SEH + qrow_s[r]) * D + d] = o[i];
+        if (r < nrows) a.part_o[((long)qrow_s[r] * a.max_chunks + id.c) * D + d] = o[i];
     }
     if (tid < nrows) {
-        a.part_m[(long)id.c * SEH + qrow_s[tid]] = m_run[tid];
-        a.part_l[(long)id.c * SEH + qrow_s[tid]] = l_run[tid];
+        const long slot = (long)qrow_s[tid] * a.max_chunks + id.c;
+        *reinterpret_cast<float2*>(a.part_ml + 2 * slot) = make_float2(m_run[tid], l_run[tid]);
     }
 }
 

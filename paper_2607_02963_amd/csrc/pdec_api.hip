@@ -6,7 +6,7 @@
 //      virtual key sequence (prefix units, then each stream's own units),
 //      each writing one partial softmax state per query row into the
 //      workspace;
-//   2. the finish pass — per (stream, kv head): merge of the row's states,
+//   2. the finish pass — per (stream, head) row: merge of the row's states,
 //      writing out and lse.
 // Nothing is allocated per call; the workspace is the caller's.
 #include <hip/hip_runtime.h>
@@ -186,8 +186,7 @@ int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_pr
     a.lse = lse;
     const size_t rows = (size_t)d->num_events * d->num_q_heads;
     a.part_o = static_cast<float*>(workspace);
-    a.part_m = a.part_o + (size_t)p.max_chunks * rows * d->head_dim;
-    a.part_l = a.part_m + (size_t)p.max_chunks * rows;
+    a.part_ml = a.part_o + (size_t)p.max_chunks * rows * d->head_dim;
     a.video_chunks = reinterpret_cast<int32_t*>(a.part_o + p.part_floats);
     a.num_videos = num_videos;
     a.num_events = d->num_events;
@@ -225,13 +224,14 @@ int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_pr
     if ((rc = launch_status()) != PDEC_OK) return rc;
     if (timer_slot >= 0 && hipEventRecord(static_cast<hipEvent_t>(g_timer_stop[timer_slot]), s) != hipSuccess)
         return PDEC_ERR_HIP;
-    const int fgrid = d->num_events * d->num_kv_heads;
+    const int fgrid = (int)rows;
+    const dim3 fblock(256);
     if (bf16) {
-        if (d->head_dim == 128) hipLaunchKernelGGL((finish_kernel<uint16_t, 128>), dim3(fgrid), dim3(1024), 0, s, a);
-        else hipLaunchKernelGGL((finish_kernel<uint16_t, 64>), dim3(fgrid), dim3(1024), 0, s, a);
+        if (d->head_dim == 128) hipLaunchKernelGGL((finish_kernel<uint16_t, 128>), dim3(fgrid), fblock, 0, s, a);
+        else hipLaunchKernelGGL((finish_kernel<uint16_t, 64>), dim3(fgrid), fblock, 0, s, a);
     } else {
-        if (d->head_dim == 128) hipLaunchKernelGGL((finish_kernel<float, 128>), dim3(fgrid), dim3(1024), 0, s, a);
-        else hipLaunchKernelGGL((finish_kernel<float, 64>), dim3(fgrid), dim3(1024), 0, s, a);
+        if (d->head_dim == 128) hipLaunchKernelGGL((finish_kernel<float, 128>), dim3(fgrid), fblock, 0, s, a);
+        else hipLaunchKernelGGL((finish_kernel<float, 64>), dim3(fgrid), fblock, 0, s, a);
     }
     return launch_status();
 }

@@ -45,9 +45,8 @@ struct StepArgs {
     const int32_t* prefix_len;  // one video: [1]; null for a ragged batch
     void* out;
     float* lse;                 // may be null
-    float* part_o;              // [max_chunks, SE*H_q, D]
-    float* part_m;              // [max_chunks, SE*H_q]
-    float* part_l;              // [max_chunks, SE*H_q]
+    float* part_o;              // [SE*H_q, max_chunks, D]: un-normalised outputs
+    float* part_ml;             // [SE*H_q, max_chunks, 2]: (reference max, normaliser)
     int32_t* video_chunks;      // [V]: chunks holding states, written by the split pass
     int num_videos;
     int num_events;             // SE
