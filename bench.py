@@ -103,12 +103,90 @@ def cpu_baseline(s):
                       f"dense-mask oracle, OpenMP over rows"}
 
 
+def run_loop(args, torch, pdec, wl):
+    """Row a6: the event-parallel decode loop (append + attention per step)
+    against the single-stream sequential decode of the same tokens.  Steps
+    after every stream has ended are not run (no stream issues a token).
+    Two timings: per-step HIP events with a 512 MB cache flush before each
+    step (outside the timed region), summed; and the whole loop back to back
+    (the 33.5 MB prefix then stays in the 256 MB MALL: "mall_hot")."""
+    lp = wl.loop_64()
+    flush = torch.empty(ROTATE_BYTES, dtype=torch.uint8, device="cuda")
+
+    def setup(lp):
+        def f(a):
+            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+        E = lp.num_events
+        d = dict(kp=f(lp.k_prefix), vp=f(lp.v_prefix), q=f(lp.q_steps), kn=f(lp.k_new), vn=f(lp.v_new),
+                 live=torch.from_numpy(lp.live_mask()).cuda(),
+                 plen=torch.tensor([lp.prefix_len], dtype=torch.int32, device="cuda"))
+        d["kc"] = torch.zeros((E, lp.cap, lp.H_kv, lp.D), dtype=torch.bfloat16, device="cuda")
+        d["vc"] = torch.zeros_like(d["kc"])
+        d["lens"] = torch.zeros(E, dtype=torch.int32, device="cuda")
+        d["out"] = torch.empty((E, lp.H_q, lp.D), dtype=torch.bfloat16, device="cuda")
+        d["lse"] = torch.empty((E, lp.H_q), dtype=torch.float32, device="cuda")
+        dims = pdec.make_dims(E, lp.H_q, lp.H_kv, lp.D, lp.cap, lp.prefix_len, pdec.PDEC_DTYPE_BF16)
+        d["ws"] = torch.empty(pdec.workspace_size(dims), dtype=torch.uint8, device="cuda")
+        d["steps"] = int(lp.eos_step.max())
+        return d
+
+    def one(d, s):
+        pdec.kv_append(d["kn"][s], d["vn"][s], d["kc"], d["vc"], d["lens"], d["live"][s])
+        pdec.attn_step(d["q"][s], d["kp"], d["vp"], d["kc"], d["vc"], d["lens"], d["plen"], out=d["out"],
+                       lse=d["lse"], workspace=d["ws"])
+
+    def timed(d):
+        d["lens"].zero_()
+        for s in range(d["steps"]):  # warm-up pass
+            one(d, s)
+        d["lens"].zero_()
+        torch.cuda.synchronize()
+        total = 0.0
+        for s in range(d["steps"]):
+            flush.fill_(s & 255)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            one(d, s)
+            e1.record()
+            e1.synchronize()
+            total += e0.elapsed_time(e1)
+        d["lens"].zero_()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for s in range(d["steps"]):
+            one(d, s)
+        e1.record()
+        torch.cuda.synchronize()
+        return total * 1e3, e0.elapsed_time(e1) * 1e3
+
+    par = setup(lp)
+    par_us, par_hot = timed(par)
+    _log(f"bench: loop {par['steps']} steps: {par_us:.1f} us flushed, {par_hot:.1f} us back to back")
+    seq = setup(lp.sequential())
+    seq_us, seq_hot = timed(seq)
+    _log(f"bench: sequential {seq['steps']} steps: {seq_us:.1f} us flushed, {seq_hot:.1f} us back to back")
+    rec = {
+        "metric": "us per event-parallel decode loop (append + attention), prefix 16384, 16 streams, EOS U{16..64}",
+        "value": round(par_us, 1), "unit": "us/loop", "n_gpus": 1, "higher_is_better": False, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": lp.name, "prefix_len": lp.prefix_len, "streams": lp.num_events, "H_q": lp.H_q,
+                   "H_kv": lp.H_kv, "head_dim": lp.D, "seed": lp.seed, "steps_run": par["steps"],
+                   "tokens": int(lp.eos_step.sum())},
+        "mall_hot_us": round(par_hot, 1),
+        "sequential": {"steps": seq["steps"], "us": round(seq_us, 1), "mall_hot_us": round(seq_hot, 1)},
+        "speedup_vs_sequential": round(seq_us / par_us, 2),
+        "tokens_per_s": round(int(lp.eos_step.sum()) / (par_us * 1e-6), 1),
+    }
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="long_32k", help="long_32k | single_8k | ragged_16 | tiny_f32")
+    ap.add_argument("--workload", default="long_32k", help="long_32k | single_8k | ragged_16 | tiny_f32 | loop_64")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MB (5 times) and exit; "
@@ -136,6 +214,9 @@ def main():
     from paper_2607_02963_amd import workloads as wl
 
     torch.cuda.set_device(0)
+    if args.workload == "loop_64":
+        run_loop(args, torch, pdec, wl)
+        return
     s = wl.STEP_WORKLOADS[args.workload]()
     ragged = s.num_videos > 1
     base = _dev_step(s, torch)
@@ -146,7 +227,8 @@ def main():
     lse = torch.empty(s.num_events, s.H_q, dtype=torch.float32, device="cuda")
     max_ev = int(s.events_per_video.max())
     max_L = int(s.prefix_lens.max())
-    dims = pdec.make_dims(s.num_events, s.H_q, s.H_kv, s.D, s.cap, max_L, pdec._dtype_code(out), s.scale, max_ev)
+    dims = pdec.make_dims(s.num_events, s.H_q, s.H_kv, s.D, s.cap, max_L, pdec._dtype_code(out), s.scale, max_ev,
+                          prefix_tokens=int(s.cu_prefix[-1]) if ragged else 0)
     ws = torch.empty(pdec.workspace_size(dims, s.num_videos), dtype=torch.uint8, device="cuda")
     path, chunk = pdec.query_plan(dims, s.num_videos)
     stream = torch.cuda.current_stream()

@@ -48,8 +48,6 @@ typedef __attribute__((ext_vector_type(4))) uint32_t u32x4_t;
 typedef __attribute__((ext_vector_type(2))) uint32_t u32x2_t;
 typedef __attribute__((ext_vector_type(4))) short s16x4_t;
 
-typedef __attribute__((address_space(3))) void lds_void_t;
-
 __device__ inline f32x4_t mfma_16x16x32(bf16x8_t a, bf16x8_t b, f32x4_t c)
 {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
@@ -92,41 +90,6 @@ __device__ inline float sum_over_groups(float x)
 // this by more than 8), and 2^(s*c - kMinRef) is never evaluated before.
 constexpr float kMinRef = -1e30f;
 
-// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
-template <int N>
-__device__ inline void wait_vmcnt()
-{
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-
-// LDS byte address of a pointer into a __shared__ array.
-__device__ inline uint32_t lds_u32(const void* p) { return (uint32_t)(uintptr_t)(lds_void_t*)p; }
-
-// One wave-wide 16-byte-per-lane DMA from global memory straight into LDS:
-// lane l's 16 bytes land at lds_base + 16 l.  Issued from inline assembly so
-// the compiler does not pair it with a conservative drain of every
-// outstanding load before later LDS reads; completion is awaited explicitly
-// with stage_barrier.  M0 (the LDS base register) is restored afterwards.
-__device__ inline void dma_16B(const void* src, uint32_t lds_base)
-{
-    uint32_t saved;
-    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %2, off\n\ts_mov_b32 m0, %0"
-                 : "=&s"(saved)
-                 : "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(src)
-                 : "memory");
-}
-
-// Wait until at most N of this wave's vector-memory operations are in flight
-// and its LDS operations are done, then barrier the work-group.  Written as
-// one asm statement so the compiler neither drains every DMA nor moves LDS
-// accesses across it.
-template <int N>
-__device__ inline void stage_barrier()
-{
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
-}
 
 template <int D, int NT, int WR, int WK>
 struct MfmaCfg {

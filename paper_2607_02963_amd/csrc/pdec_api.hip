@@ -16,6 +16,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstdlib>
+#include <type_traits>
 
 #include "pdec.h"
 
@@ -102,7 +103,7 @@ Plan make_plan(const pdec_dims* d, int num_videos)
         p.rows_per_item = tiles <= 4 ? 64 : tiles <= 8 ? 128 : 256;
     } else {
         p.shape = 0;
-        p.rows_per_item = rows_max <= 8 ? 8 : 16;
+        p.rows_per_item = 8;
     }
     p.rg_max = (int)ceil_div(rows_max, p.rows_per_item);
     // Units of the virtual key sequence of one (video, kv head): prefix units
@@ -114,6 +115,11 @@ Plan make_plan(const pdec_dims* d, int num_videos)
     const long tokens = d->prefix_tokens > 0 ? d->prefix_tokens : (long)num_videos * d->max_prefix_len;
     const long units_expected = ceil_div(tokens, kUnitKeys) + (long)d->num_events;
     long upc = ceil_div(units_expected * d->num_kv_heads * p.rg_max, kTargetItems);
+    if (path == kPathValu) {
+        // four waves per item, each taking every fourth unit: a multiple of 4
+        upc = std::max<long>(4, (units_expected * d->num_kv_heads * p.rg_max + 2 * kTargetItems) /
+                                    (4 * kTargetItems) * 4);
+    }
     upc = std::max<long>(upc, ceil_div(std::max<long>(units_max, 1), kMaxChunks));
     upc = std::max<long>(upc, 1);
     p.unit_per_chunk = (int)std::min<long>(upc, 1L << 24);
@@ -142,10 +148,12 @@ void launch_mfma(const StepArgs& a, int shape, int grid, hipStream_t s)
 }
 
 template <typename T, int D>
-void launch_valu(const StepArgs& a, int rt, int grid, hipStream_t s)
+void launch_valu(const StepArgs& a, int grid, hipStream_t s)
 {
-    if (rt == 8) hipLaunchKernelGGL((split_valu_kernel<T, D, 8>), dim3(grid), dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((split_valu_kernel<T, D, 16>), dim3(grid), dim3(256), 0, s, a);
+    if constexpr (std::is_same<T, uint16_t>::value)
+        hipLaunchKernelGGL((split_valu_bf16_kernel<D, 8>), dim3(grid), dim3(256), 0, s, a);
+    else
+        hipLaunchKernelGGL((split_valu_f32_kernel<D, 8>), dim3(grid), dim3(256), 0, s, a);
 }
 
 int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_prefix, const void* v_prefix,
@@ -215,11 +223,11 @@ int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_pr
         if (d->head_dim == 128) launch_mfma<128>(a, p.shape, grid, s);
         else launch_mfma<64>(a, p.shape, grid, s);
     } else if (bf16) {
-        if (d->head_dim == 128) launch_valu<uint16_t, 128>(a, p.rows_per_item, grid, s);
-        else launch_valu<uint16_t, 64>(a, p.rows_per_item, grid, s);
+        if (d->head_dim == 128) launch_valu<uint16_t, 128>(a, grid, s);
+        else launch_valu<uint16_t, 64>(a, grid, s);
     } else {
-        if (d->head_dim == 128) launch_valu<float, 128>(a, p.rows_per_item, grid, s);
-        else launch_valu<float, 64>(a, p.rows_per_item, grid, s);
+        if (d->head_dim == 128) launch_valu<float, 128>(a, grid, s);
+        else launch_valu<float, 64>(a, grid, s);
     }
     if ((rc = launch_status()) != PDEC_OK) return rc;
     if (timer_slot >= 0 && hipEventRecord(static_cast<hipEvent_t>(g_timer_stop[timer_slot]), s) != hipSuccess)

@@ -61,18 +61,25 @@ def test_hidden_cache_rows_and_ended_streams_never_read(poison):
 
 
 def test_prefix_rows_past_length_never_read():
+    """Prefix buffers longer than the prefix: the rows past it are zeros in
+    one run and NaN in the other (same shapes, so the same work split)."""
     s = _step()
     L = int(s.prefix_lens[0])
     d = DevStep(s)
-    o1, l1 = d.run()
     pad = 300
-    kp = torch.full((L + pad,) + tuple(d.k_prefix.shape[1:]), float("nan"), dtype=d.k_prefix.dtype, device="cuda")
-    vp = kp.clone()
-    kp[:L] = d.k_prefix
-    vp[:L] = d.v_prefix
-    o2, l2 = pdec.attn_step(d.q, kp, vp, d.k_event, d.v_event, d.event_lens, d.prefix_lens)
+
+    def padded(fill):
+        kp = torch.full((L + pad,) + tuple(d.k_prefix.shape[1:]), fill, dtype=d.k_prefix.dtype, device="cuda")
+        vp = kp.clone()
+        kp[:L] = d.k_prefix
+        vp[:L] = d.v_prefix
+        return pdec.attn_step(d.q, kp, vp, d.k_event, d.v_event, d.event_lens, d.prefix_lens)
+
+    o1, l1 = padded(0.0)
+    o2, l2 = padded(float("nan"))
     torch.cuda.synchronize()
     assert _same(o1, o2) and _same(l1, l2)
+    check("bf16", host(o2), host(l2), *oracle_ref(s))
 
 
 def test_output_and_workspace_contents_are_ignored():
