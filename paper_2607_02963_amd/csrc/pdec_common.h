@@ -93,13 +93,15 @@ __device__ inline int video_of_event(const StepArgs& a, int e)
     return lo;
 }
 
-// Work item of hardware block b.  Blocks are dispatched round-robin over the
-// 8 XCDs (block b runs on XCD b % 8), each XCD with its own L2.  Chunks are
-// dealt round-robin over the XCDs, so chunk slots a video does not fill are
-// spread evenly and no XCD gets more busy items than its share; the row
-// groups of one chunk, which read the same keys, go to the same XCD one
-// after another.  With a single row group this is the identity.  Returns -1
-// for blocks past the last item.
+// Work item of hardware block b.  Blocks are dispatched in index order,
+// round-robin over the 8 XCDs (block b runs on XCD b % 8, each XCD with its
+// own L2).  Items are numbered chunk-major (see item_id), so the slots of
+// chunks that a video may not fill (the chunk count covers every cache
+// full) come last in dispatch order: the blocks that exit at once do not
+// push a busy item into a second round on a compute unit.  The row groups of
+// one chunk, which read the same keys, go to the same XCD one after
+// another.  With a single row group this is the identity.  Returns -1 for
+// blocks past the last item.
 __device__ inline int item_of_block(const StepArgs& a, int b)
 {
     const int x = b % 8, j = b / 8;
@@ -111,15 +113,16 @@ struct ItemId {
     int v, g, c, rg;
 };
 
+// item = ((c * V + v) * H_kv + g) * rg_max + rg
 __device__ inline ItemId item_id(const StepArgs& a, int item)
 {
     ItemId id;
     id.rg = item % a.rg_max;
     item /= a.rg_max;
-    id.c = item % a.max_chunks;
-    item /= a.max_chunks;
     id.g = item % a.H_kv;
-    id.v = item / a.H_kv;
+    item /= a.H_kv;
+    id.v = item % a.num_videos;
+    id.c = item / a.num_videos;
     return id;
 }
 
