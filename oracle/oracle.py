@@ -53,7 +53,7 @@ def _load():
             fn = getattr(lib, f"oracle_attn_step_{sfx}")
             fn.restype = ctypes.c_int
             fn.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
-                           ctypes.c_int, ctypes.c_int, ctypes.c_double, ctypes.c_int,
+                           ctypes.c_int, ctypes.c_int, ctypes.c_double, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int]
@@ -62,7 +62,8 @@ def _load():
             fn.argtypes = [ctypes.c_int] * 7 + [ctypes.c_double, ctypes.c_int] + [ctypes.c_void_p] * 8 + [ctypes.c_int]
             fn = getattr(lib, f"oracle_build_mask_{sfx}")
             fn.restype = ctypes.c_int
-            fn.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+            fn.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
+                           ctypes.c_void_p]
             getattr(lib, f"oracle_max_threads_{sfx}").restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -86,7 +87,7 @@ def _c(a, dtype=None):
 
 def attn_step(q, k_prefix, v_prefix, k_event, v_event, event_lens, cu_prefix, cu_events,
               scale: float = 0.0, row_select=None, want_probs: bool = False, threads: int = 0,
-              precision: str = "f64"):
+              precision: str = "f64", plan_mask: int = 0, plan_per_stream: int = 0):
     """One decode step over a batch of videos.
 
     Shapes: q [SE,H_q,D]; k/v_prefix [SL,H_kv,D]; k/v_event [SE,cap,H_kv,D];
@@ -95,6 +96,9 @@ def attn_step(q, k_prefix, v_prefix, k_event, v_event, event_lens, cu_prefix, cu
     lse [SE,H_q]) in the oracle precision, plus the attention weights over the
     unified key sequence [SE,H_q,U] when ``want_probs`` (one video only).
     Rows not selected by ``row_select`` ([SE,H_q] bool) are returned as NaN.
+    ``plan_mask`` 1 with ``plan_per_stream`` T > 0 selects the "self G-token
+    only" variant of Table 8 (each stream sees only its own run of T tokens
+    in the last E*T prefix tokens of its video).
     """
     lib = _load()
     real = np.float64 if precision == "f64" else np.float32
@@ -118,8 +122,8 @@ def attn_step(q, k_prefix, v_prefix, k_event, v_event, event_lens, cu_prefix, cu
         U = int(cu_prefix[1] - cu_prefix[0]) + SE * cap
         probs = np.zeros((SE, H_q, U), dtype=real)
     sel = None if row_select is None else _c(row_select, np.uint8)
-    rc = fn(V, _ptr(cu_prefix), _ptr(cu_events), H_q, H_kv, D, cap, float(scale), dt,
-            _ptr(q), _ptr(k_prefix), _ptr(v_prefix), _ptr(k_event), _ptr(v_event), _ptr(event_lens),
+    rc = fn(V, _ptr(cu_prefix), _ptr(cu_events), H_q, H_kv, D, cap, float(scale), dt, int(plan_mask),
+            int(plan_per_stream), _ptr(q), _ptr(k_prefix), _ptr(v_prefix), _ptr(k_event), _ptr(v_event), _ptr(event_lens),
             _ptr(sel), _ptr(out), _ptr(lse), _ptr(probs), int(threads))
     if rc != 0:
         raise ValueError("oracle_attn_step rejected its arguments")
@@ -151,12 +155,14 @@ def decode_loop(k_prefix, v_prefix, q_steps, k_new, v_new, eos_step, cap: int, s
     return out, lse
 
 
-def build_mask(L: int, E: int, cap: int, n) -> np.ndarray:
-    """The explicit [E, L + E*cap] visibility matrix the oracle uses (§3.4, Fig. 3)."""
+def build_mask(L: int, E: int, cap: int, n, plan_mask: int = 0, plan_per_stream: int = 0) -> np.ndarray:
+    """The explicit [E, L + E*cap] visibility matrix the oracle uses (§3.4, Fig. 3;
+    with ``plan_mask``, the "self G-token only" variant of Table 8)."""
     lib = _load()
     n = _c(n, np.int32)
     mask = np.zeros((E, L + E * cap), dtype=np.uint8)
-    if lib.oracle_build_mask_f64(int(L), int(E), int(cap), _ptr(n), _ptr(mask)) != 0:
+    if lib.oracle_build_mask_f64(int(L), int(E), int(cap), _ptr(n), int(plan_mask), int(plan_per_stream),
+                                 _ptr(mask)) != 0:
         raise ValueError("bad mask arguments")
     return mask.astype(bool)
 

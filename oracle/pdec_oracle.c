@@ -30,6 +30,11 @@
  *   - scores are scale * <q, k>, scale = 1/sqrt(D) unless given.
  *   - grouped-query heads: query head h reads key/value head h / (H_q/H_kv).
  *   - lse is the natural-log log-sum-exp of the scaled scores.
+ *   - the "self G-token only" variant of Table 8 (a branch sees, among the
+ *     global plan tokens, only its own G^i) needs to know where the plan
+ *     tokens are: the plan segment is taken as the last E*T prefix tokens,
+ *     stream f's tokens being the f-th run of T of them (T tokens per
+ *     stream, in stream order).
  *
  * Arithmetic type: `real`, double by default.  The same source compiled with
  * -DORACLE_REAL=float gives the fp32 variant (functions suffixed _f32), used
@@ -79,16 +84,23 @@ static real load_elem(const void* base, size_t idx, int dtype)
  *     j =  L + f * cap + t        : row t of stream f's cache   -> visible
  *                                    iff f == e and t < n_e
  * Streams with n_e == 0 get an all-zero row (no query this step).
+ * plan_mask != 0 with plan_T > 0 selects the "self G-token only" variant of
+ * Table 8: prefix token j >= L - E*plan_T (the plan segment) is visible to
+ * stream e only if it lies in e's own run of plan_T tokens.  The plan segment
+ * must fit in the prefix (E*plan_T <= L).
  */
-int ORACLE_FN(oracle_build_mask)(int L, int E, int cap, const int32_t* n, uint8_t* mask)
+int ORACLE_FN(oracle_build_mask)(int L, int E, int cap, const int32_t* n, int plan_mask, int plan_T, uint8_t* mask)
 {
-    if (L < 0 || E < 0 || cap < 0 || (!mask && E > 0)) return -1;
+    if (L < 0 || E < 0 || cap < 0 || plan_T < 0 || (!mask && E > 0)) return -1;
+    const long plan0 = (plan_mask && plan_T > 0) ? (long)L - (long)E * plan_T : (long)L;
+    if (plan0 < 0) return -1;
     const long U = (long)L + (long)E * cap;
     for (int e = 0; e < E; ++e) {
         uint8_t* row = mask + (long)e * U;
         memset(row, 0, (size_t)U);
         if (n[e] <= 0) continue;
         for (long j = 0; j < L; ++j) row[j] = 1;                  /* shared prefix and plan tokens */
+        for (long j = plan0; j < L; ++j) row[j] = (j - plan0) / plan_T == e; /* self G-token only */
         for (int f = 0; f < E; ++f)
             for (int t = 0; t < cap; ++t)
                 if (f == e && t < n[e]) row[L + (long)f * cap + t] = 1; /* own stream only */
@@ -106,6 +118,8 @@ int ORACLE_FN(oracle_build_mask)(int L, int E, int cap, const int32_t* n, uint8_
  *   cap                   rows per stream cache
  *   scale                 score scale (<= 0 selects 1/sqrt(D))
  *   dtype                 0: float32 tensors, 1: bfloat16 tensors (stored as uint16 bits)
+ *   plan_mask, plan_T     0, 0: the full design; 1, T: "self G-token only" with T
+ *                         plan tokens per stream (see oracle_build_mask)
  *   q        [SE, H_q, D]            SE = cu_events[V]
  *   k_prefix [SL, H_kv, D]           SL = cu_prefix[V]
  *   v_prefix [SL, H_kv, D]
@@ -122,7 +136,7 @@ int ORACLE_FN(oracle_build_mask)(int L, int E, int cap, const int32_t* n, uint8_
  */
 int ORACLE_FN(oracle_attn_step)(int num_videos, const int32_t* cu_prefix, const int32_t* cu_events,
                                 int H_q, int H_kv, int D, int cap, double scale, int dtype,
-                                const void* q, const void* k_prefix, const void* v_prefix,
+                                int plan_mask, int plan_T, const void* q, const void* k_prefix, const void* v_prefix,
                                 const void* k_event, const void* v_event, const int32_t* n,
                                 const uint8_t* row_select, real* out, real* lse, real* probs,
                                 int num_threads)
@@ -146,7 +160,10 @@ int ORACLE_FN(oracle_attn_step)(int num_videos, const int32_t* cu_prefix, const 
         const long U = (long)L + (long)E * cap;
         uint8_t* mask = (uint8_t*)malloc((size_t)(E > 0 ? E : 1) * (size_t)(U > 0 ? U : 1));
         if (!mask) return -1;
-        ORACLE_FN(oracle_build_mask)(L, E, cap, n + e0, mask);
+        if (ORACLE_FN(oracle_build_mask)(L, E, cap, n + e0, plan_mask, plan_T, mask) != 0) {
+            free(mask);
+            return -1;
+        }
 
         int bad = 0;
 #pragma omp parallel for schedule(dynamic, 1)
@@ -254,7 +271,7 @@ int ORACLE_FN(oracle_decode_loop)(int steps, int E, int H_q, int H_kv, int D, in
         }
         if (rc) break;
         const unsigned char* qs = (const unsigned char*)q_steps + (size_t)s * E * H_q * D * esz;
-        rc = ORACLE_FN(oracle_attn_step)(1, cu_prefix, cu_events, H_q, H_kv, D, cap, scale, dtype, qs,
+        rc = ORACLE_FN(oracle_attn_step)(1, cu_prefix, cu_events, H_q, H_kv, D, cap, scale, dtype, 0, 0, qs,
                                          k_prefix, v_prefix, kc, vc, n, NULL,
                                          out + (size_t)s * E * H_q * D, lse + (size_t)s * E * H_q, NULL,
                                          num_threads);

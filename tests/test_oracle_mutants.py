@@ -28,6 +28,9 @@ MUTANTS = {
     "normaliser_dropped": ("const real p = r_exp(s[j] - m) / l;", "const real p = r_exp(s[j] - m);"),
     "ended_stream_sees_prefix": ("if (n[e] <= 0) continue;", "if (n[e] < 0) continue;"),
     "loop_no_eos": ("if (s < eos_step[e]) {", "if (1) {"),
+    "plan_group_modulo": ("row[j] = (j - plan0) / plan_T == e;", "row[j] = (j - plan0) % E == e;"),
+    "plan_start_off_by_one": ("(long)L - (long)E * plan_T : (long)L;", "(long)L - (long)E * plan_T + 1 : (long)L;"),
+    "plan_mask_ignored": ("for (long j = plan0; j < L; ++j)", "for (long j = L; j < L; ++j)"),
 }
 
 

@@ -81,6 +81,115 @@ def test_mask_matches_hand_written_table(case):
     assert np.array_equal(got, want)
 
 
+def _golden_self_plan():
+    cases, cur = [], None
+    with open(os.path.join(GOLDEN, "mask_self_plan.txt")) as f:
+        for line in f:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            if line.startswith("case"):
+                kv = dict(tok.split("=") for tok in line.split()[1:])
+                cur = dict(L=int(kv["L"]), E=int(kv["E"]), cap=int(kv["cap"]), T=int(kv["T"]),
+                           n=[int(x) for x in kv["n"].split(",")], rows=[])
+                cases.append(cur)
+            else:
+                cur["rows"].append([int(x) for x in line.split()])
+    return cases
+
+
+@pytest.mark.parametrize("case", _golden_self_plan(), ids=lambda c: f"L{c['L']}E{c['E']}T{c['T']}")
+def test_self_plan_mask_matches_hand_written_table(case):
+    """Table 8, "self G-token only": each stream sees only its own run of
+    plan tokens at the end of the prefix."""
+    got = oracle.build_mask(case["L"], case["E"], case["cap"], case["n"], plan_mask=1, plan_per_stream=case["T"])
+    want = np.array(case["rows"], dtype=bool)
+    assert got.shape == want.shape
+    assert np.array_equal(got, want)
+
+
+def test_self_plan_rejects_a_segment_longer_than_the_prefix():
+    with pytest.raises(ValueError):
+        oracle.build_mask(3, 2, 1, [1, 1], plan_mask=1, plan_per_stream=2)
+
+
+def _self_plan_case(seed, L=40, E=3, T=4, H_q=4, H_kv=2, D=16, dtype="f32"):
+    return wl.make_step(dtype=dtype, H_q=H_q, H_kv=H_kv, D=D, prefix_lens=(L,), events_per_video=(E,),
+                        own_len_range=(0, 6), sigma=1.0, seed=seed)
+
+
+def test_self_plan_equals_decoding_over_the_reduced_prefix():
+    """Masking the other streams' plan tokens gives exactly what a stream
+    gets when those tokens are absent: each stream against the prefix with
+    only its own run of plan tokens kept, decoded alone."""
+    E, T = 3, 4
+    s = _self_plan_case(3, E=E, T=T)
+    L = int(s.prefix_lens[0])
+    out, lse = _single(s.q, s.k_prefix, s.v_prefix, s.k_event, s.v_event, s.event_lens, plan_mask=1,
+                       plan_per_stream=T)
+    p0 = L - E * T
+    for f in range(E):
+        keep = np.r_[0:p0, p0 + f * T:p0 + (f + 1) * T]
+        o1, l1 = _single(s.q[f:f + 1], s.k_prefix[keep], s.v_prefix[keep], s.k_event[f:f + 1],
+                         s.v_event[f:f + 1], s.event_lens[f:f + 1])
+        if s.event_lens[f] == 0:
+            assert np.all(out[f] == 0) and np.all(np.isneginf(lse[f]))
+            continue
+        np.testing.assert_allclose(out[f], o1[0], rtol=0, atol=1e-12)
+        np.testing.assert_allclose(lse[f], l1[0], rtol=0, atol=1e-12)
+
+
+def test_self_plan_zero_keys_average_the_visible_values():
+    """k = 0 under the self-plan mask: out is the mean of the values in the
+    audio-visual part, the stream's own plan run and its own rows; lse =
+    ln(count).  Computed directly in numpy."""
+    E, T = 3, 2
+    s = _self_plan_case(4, L=23, E=E, T=T, H_q=2, H_kv=1, D=8)
+    s.k_prefix[:] = 0
+    s.k_event[:] = 0
+    L = int(s.prefix_lens[0])
+    out, lse = _single(s.q, s.k_prefix, s.v_prefix, s.k_event, s.v_event, s.event_lens, plan_mask=1,
+                       plan_per_stream=T)
+    p0 = L - E * T
+    for f in range(E):
+        n = int(s.event_lens[f])
+        if n == 0:
+            continue
+        vis = np.concatenate([s.v_prefix[:p0, 0], s.v_prefix[p0 + f * T:p0 + (f + 1) * T, 0],
+                              s.v_event[f, :n, 0]]).astype(np.float64)
+        for h in range(2):
+            np.testing.assert_allclose(out[f, h], vis.mean(axis=0), atol=1e-12)
+            assert abs(lse[f, h] - math.log(p0 + T + n)) < 1e-12
+
+
+def test_self_plan_without_plan_tokens_is_the_full_design():
+    s = _self_plan_case(5)
+    o0, l0 = _single(s.q, s.k_prefix, s.v_prefix, s.k_event, s.v_event, s.event_lens)
+    o1, l1 = _single(s.q, s.k_prefix, s.v_prefix, s.k_event, s.v_event, s.event_lens, plan_mask=1,
+                     plan_per_stream=0)
+    o2, l2 = _single(s.q, s.k_prefix, s.v_prefix, s.k_event, s.v_event, s.event_lens, plan_mask=0,
+                     plan_per_stream=4)
+    assert np.array_equal(o0, o1) and np.array_equal(l0, l1)
+    assert np.array_equal(o0, o2) and np.array_equal(l0, l2)
+
+
+def test_self_plan_stream_permutation_moves_the_plan_runs():
+    """Permuting the streams together with their plan runs permutes the
+    outputs."""
+    E, T = 4, 3
+    s = _self_plan_case(6, L=50, E=E, T=T)
+    L = int(s.prefix_lens[0])
+    out, lse = _single(s.q, s.k_prefix, s.v_prefix, s.k_event, s.v_event, s.event_lens, plan_mask=1,
+                       plan_per_stream=T)
+    perm = np.array([2, 0, 3, 1])
+    p0 = L - E * T
+    rows = np.r_[0:p0, np.concatenate([np.arange(p0 + f * T, p0 + (f + 1) * T) for f in perm])]
+    out_p, lse_p = _single(s.q[perm], s.k_prefix[rows], s.v_prefix[rows], s.k_event[perm], s.v_event[perm],
+                           s.event_lens[perm], plan_mask=1, plan_per_stream=T)
+    np.testing.assert_allclose(out_p, out[perm], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(lse_p, lse[perm], rtol=0, atol=1e-12)
+
+
 # ---------------------------------------------------------------------------
 # (a) one stream is ordinary causal decoding (Eq. 1)
 # ---------------------------------------------------------------------------
