@@ -71,12 +71,12 @@ def split_kernel_bytes(s) -> int:
 PROFILE = os.path.join(ROOT, "profiles", "split_finish__long_L32768_E32__hbm_counters.txt")
 
 
-def measured_traffic(workload_name: str):
+def measured_traffic(workload_name: str, plan_mask: str):
     """HBM bytes per split-kernel launch from the stored FETCH_SIZE/WRITE_SIZE
     counters, scaled by the copy-kernel calibration; None unless they were
     taken on this workload with the kernels as built now."""
     from paper_2607_02963_amd import _build
-    if workload_name != "long_L32768_E32" or not os.path.exists(PROFILE):
+    if workload_name != "long_L32768_E32" or plan_mask != "full" or not os.path.exists(PROFILE):
         return None
     fields = {}
     with open(PROFILE) as fh:
@@ -89,14 +89,14 @@ def measured_traffic(workload_name: str):
     return int(fields["traffic_bytes_per_launch"])
 
 
-def cpu_baseline(s):
+def cpu_baseline(s, plan):
     """The oracle (as it stands) on the host cores: one full step, all rows."""
     sys.path.insert(0, os.path.join(ROOT, "oracle"))
     import oracle
     threads = oracle.max_threads()
     t0 = time.perf_counter()
     oracle.attn_step(s.q, s.k_prefix, s.v_prefix, s.k_event, s.v_event, s.event_lens, s.cu_prefix, s.cu_events,
-                     scale=s.scale, threads=threads)
+                     scale=s.scale, threads=threads, **plan)
     dt = time.perf_counter() - t0
     return {"value": round(dt * 1e6, 1), "unit": "us/step", "cores": threads, "kind": "oracle",
             "sample": f"one full step of {s.name}: all {s.num_events * s.H_q} (stream, head) rows, float64 "
@@ -188,6 +188,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="long_32k", help="long_32k | single_8k | ragged_16 | tiny_f32 | loop_64")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--plan-mask", choices=("full", "self"), default="full",
+                    help="full: every stream sees all plan tokens (the full design); self: each stream sees only "
+                         "its own run of the workload's plan tokens (Table 8 'self G-token only')")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MB (5 times) and exit; "
                          "used to calibrate the HBM byte counters")
@@ -219,6 +222,13 @@ def main():
         return
     s = wl.STEP_WORKLOADS[args.workload]()
     ragged = s.num_videos > 1
+    plan = dict(plan_mask=0, plan_per_stream=0)
+    if args.plan_mask == "self":
+        if ragged or "prefix_split" not in s.meta:
+            print(json.dumps({"error": f"--plan-mask self needs a one-video workload with plan tokens; "
+                                       f"{s.name} has none"}))
+            sys.exit(2)
+        plan = dict(plan_mask=1, plan_per_stream=s.meta["prefix_split"][1] // s.num_events)
     base = _dev_step(s, torch)
     set_bytes = sum(t.numel() * t.element_size() for t in base.values())
     nsets = max(1, math.ceil(ROTATE_BYTES / set_bytes))
@@ -228,7 +238,7 @@ def main():
     max_ev = int(s.events_per_video.max())
     max_L = int(s.prefix_lens.max())
     dims = pdec.make_dims(s.num_events, s.H_q, s.H_kv, s.D, s.cap, max_L, pdec._dtype_code(out), s.scale, max_ev,
-                          prefix_tokens=int(s.cu_prefix[-1]) if ragged else 0)
+                          prefix_tokens=int(s.cu_prefix[-1]) if ragged else 0, **plan)
     ws = torch.empty(pdec.workspace_size(dims, s.num_videos), dtype=torch.uint8, device="cuda")
     path, chunk = pdec.query_plan(dims, s.num_videos)
     stream = torch.cuda.current_stream()
@@ -238,10 +248,10 @@ def main():
         if ragged:
             pdec.attn_step_ragged(d["q"], d["k_prefix"], d["v_prefix"], d["cu_prefix"], d["k_event"], d["v_event"],
                                   d["event_lens"], d["cu_events"], max_prefix_len=max_L, max_events_per_video=max_ev,
-                                  out=out, lse=lse, workspace=ws, scale=s.scale, stream=stream)
+                                  out=out, lse=lse, workspace=ws, scale=s.scale, stream=stream, **plan)
         else:
             pdec.attn_step(d["q"], d["k_prefix"], d["v_prefix"], d["k_event"], d["v_event"], d["event_lens"],
-                           d["prefix_lens"], out=out, lse=lse, workspace=ws, scale=s.scale, stream=stream)
+                           d["prefix_lens"], out=out, lse=lse, workspace=ws, scale=s.scale, stream=stream, **plan)
 
     _log(f"bench: workload {s.name} path={path} chunk={chunk} sets={nsets} x {set_bytes / 1e6:.1f} MB")
     for i in range(args.warmup):
@@ -288,18 +298,19 @@ def main():
         "data": "synthetic",
         "config": {"workload": s.name, "videos": s.num_videos, "prefix_len": max_L if not ragged else int(s.cu_prefix[-1]),
                    "events": s.num_events, "H_q": s.H_q, "H_kv": s.H_kv, "head_dim": s.D, "seed": s.seed,
-                   "kernel_path": {1: "valu", 2: "mfma"}[path], "chunk_keys": chunk},
+                   "kernel_path": {1: "valu", 2: "mfma"}[path], "chunk_keys": chunk, "plan_mask": args.plan_mask,
+                   "plan_tokens_per_stream": plan["plan_per_stream"]},
         "achieved_GBps": round(gbps, 1),
         "hbm_peak_frac": round(gbps / HBM_PEAK_GBPS, 4),
         "algorithmic_bytes_per_step": alg,
         "tokens_per_s": round(live / (ms * 1e-3), 1),
         "roofline": {"bound": "hbm", "achieved": round(kgbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(kgbps / HBM_PEAK_GBPS, 4), "traffic": measured_traffic(s.name),
+                     "frac": round(kgbps / HBM_PEAK_GBPS, 4), "traffic": measured_traffic(s.name, args.plan_mask),
                      "kernel": "split pass (shared prefix + stream rows)", "kernel_us": round(split_ms * 1e3, 3),
                      "kernel_algorithmic_bytes": kbytes},
     }
     if not args.no_cpu_baseline:
-        rec["cpu_baseline"] = cpu_baseline(s)
+        rec["cpu_baseline"] = cpu_baseline(s, plan)
     print(json.dumps(rec), flush=True)
 
 

@@ -73,6 +73,17 @@ typedef struct pdec_dims {
     float softmax_scale;          /* <= 0 selects 1/sqrt(head_dim)                               */
     int64_t prefix_tokens;        /* prefix rows over the whole batch (sizing hint for the work  */
                                   /* split); 0 means num_videos * max_prefix_len                 */
+    int32_t plan_mask;            /* 0: every stream sees the whole prefix, plan tokens included */
+                                  /* (§3.4, the full design).  1: the "self G-token only" mask   */
+                                  /* of Table 8: of the plan segment a stream sees only its own  */
+                                  /* global tokens                                               */
+    int32_t plan_tokens_per_stream; /* T, used when plan_mask = 1: the plan segment of a video  */
+                                  /* with E streams is its last E*T prefix tokens, stream f's    */
+                                  /* global tokens being the f-th run of T; E counts every      */
+                                  /* stream slot of the video, ended ones included.  The mask   */
+                                  /* is meant for E*T <= L; beyond that the runs keep their     */
+                                  /* places counted from L - E*T and the parts before prefix    */
+                                  /* key 0 do not exist.  0 means no plan segment.  Must be >= 0 */
 } pdec_dims;
 
 /* Human-readable text of a pdec_status code.  Never NULL. */

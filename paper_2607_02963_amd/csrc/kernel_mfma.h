@@ -121,7 +121,7 @@ __device__ inline int k_off(int key, int ch) { return key * (2 * D) + 16 * (ch ^
 template <int D>
 __device__ inline int v_off(int key, int ch) { return key * (2 * D) + 16 * (ch ^ ((2 * key) & 6)); }
 
-template <int D, int NT, int WR, int WK>
+template <int D, int NT, int WR, int WK, bool PLAN>
 __global__ __launch_bounds__(512) void split_mfma_kernel(StepArgs a)
 {
     using C = MfmaCfg<D, NT, WR, WK>;
@@ -245,8 +245,9 @@ __global__ __launch_bounds__(512) void split_mfma_kernel(StepArgs a)
     }
 
     // One 32-key block of this wave: S^T, online softmax, O^T += V^T P^T.
-    // MASKED: keys past nk and, for an own unit, rows of other streams are
-    // excluded; the unmasked form serves every full prefix unit.
+    // MASKED: keys past nk and keys owned by another stream (an own unit, or
+    // a plan key under the self-only mask) are excluded; the unmasked form
+    // serves every full prefix unit before the plan segment.
     auto block = [&](auto masked_tag, const unsigned char* kbuf, const unsigned char* vbuf, int kb,
                      const UnitInfo& ui) {
         constexpr bool MASKED = decltype(masked_tag)::value;
@@ -264,15 +265,33 @@ __global__ __launch_bounds__(512) void split_mfma_kernel(StepArgs a)
             }
         }
         if constexpr (MASKED) {
+            // a prefix unit reaching into the plan segment (self-only mask)
+            bool plan_unit = false;
+            if constexpr (PLAN) plan_unit = __builtin_amdgcn_readfirstlane(ui.stream < 0 && ui.k0 + kUnit > vi.plan0);
+            if (plan_unit) {
 #pragma unroll
-            for (int kt = 0; kt < 2; ++kt)
+                for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const bool kout = kb + 16 * kt + 4 * lg + i >= ui.nk;
+                    for (int i = 0; i < 4; ++i) {
+                        const int kj = kb + 16 * kt + 4 * lg + i;
+                        const bool kout = kj >= ui.nk;
 #pragma unroll
-                    for (int nt = 0; nt < NT; ++nt)
-                        if (kout || (ui.stream >= 0 && lane_stream[nt] != ui.stream)) s[kt][nt][i] = kNegInf;
-                }
+                        for (int nt = 0; nt < NT; ++nt) {
+                            const bool hide = kout | plan_key_hidden(a, vi, ui.k0 + kj, lane_stream[nt]);
+                            s[kt][nt][i] = hide ? kNegInf : s[kt][nt][i];
+                        }
+                    }
+            } else {
+#pragma unroll
+                for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const bool kout = kb + 16 * kt + 4 * lg + i >= ui.nk;
+#pragma unroll
+                        for (int nt = 0; nt < NT; ++nt)
+                            if (kout || (ui.stream >= 0 && lane_stream[nt] != ui.stream)) s[kt][nt][i] = kNegInf;
+                    }
+            }
         }
         // block max per row; rows whose max rose by more than 8 re-reference
         float mt[NT];
@@ -344,7 +363,7 @@ __global__ __launch_bounds__(512) void split_mfma_kernel(StepArgs a)
         const unsigned char* kbuf = lds + (st % C::NSTAGE) * C::STAGE;
         const unsigned char* vbuf = kbuf + C::STAGE_K;
         if (wave_has_rows) {
-            if (ui.stream < 0 && ui.nk == kUnit) {
+            if (ui.stream < 0 && ui.nk == kUnit && (!PLAN || ui.k0 + kUnit <= vi.plan0)) {
 #pragma unroll
                 for (int b = 0; b < C::KW / 32; ++b) block(std::false_type{}, kbuf, vbuf, kg * C::KW + 32 * b, ui);
             } else {

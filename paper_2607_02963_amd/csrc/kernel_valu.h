@@ -122,6 +122,7 @@ __device__ inline UnitInfo uniform_unit(const UnitInfo& x)
                        (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)off));
     y.nk = __builtin_amdgcn_readfirstlane(x.nk);
     y.stream = __builtin_amdgcn_readfirstlane(x.stream);
+    y.k0 = __builtin_amdgcn_readfirstlane(x.k0);
     return y;
 }
 
@@ -245,7 +246,7 @@ __device__ inline void valu_merge_write(const StepArgs& a, const ValuItem& it, i
 
 // ----------------------------------------------------------------------------
 // bf16: key rows split over lanes, everything in registers.
-template <int D, int RT>
+template <int D, int RT, bool PLAN>
 __global__ __launch_bounds__(256) void split_valu_bf16_kernel(StepArgs a)
 {
     constexpr int NW = 4;
@@ -383,13 +384,15 @@ __global__ __launch_bounds__(256) void split_valu_bf16_kernel(StepArgs a)
             // ---- softmax per row, lane = key; P packed as bf16 pairs ----
             {
                 const bool kvalid = lane < nk;
+                const bool plan_unit = PLAN && ui.stream < 0 && ui.k0 + kUnit > it.vi.plan0;  // self-only mask
                 const float4 x0 = *reinterpret_cast<const float4*>(sw + lane * RT);
                 const float4 x1 = *reinterpret_cast<const float4*>(sw + lane * RT + 4);
                 const float sx[RT] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
                 uint32_t pv[RT];
 #pragma unroll
                 for (int r = 0; r < RT; ++r) {
-                    const bool row_sees = row_stream[r] != -2 && (ui.stream < 0 || row_stream[r] == ui.stream);
+                    bool row_sees = row_stream[r] != -2 && (ui.stream < 0 || row_stream[r] == ui.stream);
+                    if (plan_unit) row_sees = row_sees & !plan_key_hidden(a, it.vi, ui.k0 + lane, row_stream[r]);
                     const float x = (kvalid && row_sees) ? sx[r] * c : kNegInf;
                     const float p = row_softmax<DPL>(x, m_ref[r], l_lane[r], o[r]);
                     const uint32_t bits = bf16_bits_rne(p);
@@ -435,7 +438,7 @@ __global__ __launch_bounds__(256) void split_valu_bf16_kernel(StepArgs a)
 
 // ----------------------------------------------------------------------------
 // float32, direct loads.
-template <int D, int RT>
+template <int D, int RT, bool PLAN>
 __global__ __launch_bounds__(256) void split_valu_f32_kernel(StepArgs a)
 {
     constexpr int NW = 4;
@@ -527,10 +530,12 @@ __global__ __launch_bounds__(256) void split_valu_f32_kernel(StepArgs a)
         // ---- softmax per row, lane = key ----
         {
             const bool kvalid = lane < nk;
+            const bool plan_unit = PLAN && ui.stream < 0 && ui.k0 + kUnit > it.vi.plan0;  // self-only mask
             float pv[RT];
 #pragma unroll
             for (int r = 0; r < RT; ++r) {
-                const bool row_sees = row_stream[r] != -2 && (ui.stream < 0 || row_stream[r] == ui.stream);
+                bool row_sees = row_stream[r] != -2 && (ui.stream < 0 || row_stream[r] == ui.stream);
+                if (plan_unit) row_sees = row_sees & !plan_key_hidden(a, it.vi, ui.k0 + lane, row_stream[r]);
                 const float x = (kvalid && row_sees) ? sx[r] * c : kNegInf;
                 pv[r] = row_softmax<DPL>(x, m_ref[r], l_lane[r], o[r]);
             }

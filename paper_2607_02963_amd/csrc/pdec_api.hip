@@ -69,7 +69,8 @@ int validate_dims(const pdec_dims* d, int num_videos)
     if (!d) return PDEC_ERR_INVALID_ARG;
     if (num_videos < 1 || d->num_events < 1 || d->num_q_heads < 1 || d->num_kv_heads < 1 ||
         d->num_q_heads % d->num_kv_heads != 0 || d->event_cap < 1 || d->max_prefix_len < 0 ||
-        d->max_events_per_video < 0 || d->max_events_per_video > d->num_events || d->prefix_tokens < 0)
+        d->max_events_per_video < 0 || d->max_events_per_video > d->num_events || d->prefix_tokens < 0 ||
+        d->plan_mask < 0 || d->plan_mask > 1 || d->plan_tokens_per_stream < 0)
         return PDEC_ERR_INVALID_ARG;
     if (d->dtype != PDEC_DTYPE_F32 && d->dtype != PDEC_DTYPE_BF16) return PDEC_ERR_UNSUPPORTED;
     if (d->head_dim != 64 && d->head_dim != 128) return PDEC_ERR_UNSUPPORTED;
@@ -78,6 +79,9 @@ int validate_dims(const pdec_dims* d, int num_videos)
     // call has all streams in one video
     if (events_per_video(d) > kMaxStreamsPerVideo) return PDEC_ERR_UNSUPPORTED;
     if (num_videos == 1 && d->num_events > kMaxStreamsPerVideo) return PDEC_ERR_UNSUPPORTED;
+    // the plan segment's bounds (E*T keys) are 32-bit on the device
+    if (d->plan_mask && (long)d->plan_tokens_per_stream * events_per_video(d) > (1L << 30))
+        return PDEC_ERR_UNSUPPORTED;
     // index arithmetic inside the kernels is 32-bit for row counts
     if ((long)d->num_events * d->num_q_heads > (1L << 30)) return PDEC_ERR_UNSUPPORTED;
     return PDEC_OK;
@@ -137,23 +141,39 @@ int launch_status()
     return e == hipSuccess ? PDEC_OK : PDEC_ERR_HIP;
 }
 
+template <int D, bool PLAN>
+void launch_mfma_shape(const StepArgs& a, int shape, int grid, hipStream_t s)
+{
+    switch (shape) {
+    case 1: hipLaunchKernelGGL((split_mfma_kernel<D, 1, 4, 2, PLAN>), dim3(grid), dim3(512), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((split_mfma_kernel<D, 2, 4, 2, PLAN>), dim3(grid), dim3(512), 0, s, a); break;
+    default: hipLaunchKernelGGL((split_mfma_kernel<D, 2, 8, 1, PLAN>), dim3(grid), dim3(512), 0, s, a); break;
+    }
+}
+
+// The self-only plan mask has kernels of its own, so that the full design's
+// inner loop carries none of its tests.
 template <int D>
 void launch_mfma(const StepArgs& a, int shape, int grid, hipStream_t s)
 {
-    switch (shape) {
-    case 1: hipLaunchKernelGGL((split_mfma_kernel<D, 1, 4, 2>), dim3(grid), dim3(512), 0, s, a); break;
-    case 2: hipLaunchKernelGGL((split_mfma_kernel<D, 2, 4, 2>), dim3(grid), dim3(512), 0, s, a); break;
-    default: hipLaunchKernelGGL((split_mfma_kernel<D, 2, 8, 1>), dim3(grid), dim3(512), 0, s, a); break;
-    }
+    if (a.plan_T > 0) launch_mfma_shape<D, true>(a, shape, grid, s);
+    else launch_mfma_shape<D, false>(a, shape, grid, s);
+}
+
+template <typename T, int D, bool PLAN>
+void launch_valu_kernel(const StepArgs& a, int grid, hipStream_t s)
+{
+    if constexpr (std::is_same<T, uint16_t>::value)
+        hipLaunchKernelGGL((split_valu_bf16_kernel<D, 8, PLAN>), dim3(grid), dim3(256), 0, s, a);
+    else
+        hipLaunchKernelGGL((split_valu_f32_kernel<D, 8, PLAN>), dim3(grid), dim3(256), 0, s, a);
 }
 
 template <typename T, int D>
 void launch_valu(const StepArgs& a, int grid, hipStream_t s)
 {
-    if constexpr (std::is_same<T, uint16_t>::value)
-        hipLaunchKernelGGL((split_valu_bf16_kernel<D, 8>), dim3(grid), dim3(256), 0, s, a);
-    else
-        hipLaunchKernelGGL((split_valu_f32_kernel<D, 8>), dim3(grid), dim3(256), 0, s, a);
+    if (a.plan_T > 0) launch_valu_kernel<T, D, true>(a, grid, s);
+    else launch_valu_kernel<T, D, false>(a, grid, s);
 }
 
 int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_prefix, const void* v_prefix,
@@ -212,6 +232,7 @@ int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_pr
     a.items_per_xcd = (int)(p.rg_max * ceil_div(p.n_items / p.rg_max, 8));
     const float scale = d->softmax_scale > 0.f ? d->softmax_scale : 1.f / std::sqrt((float)d->head_dim);
     a.qscale = scale * 1.4426950408889634f;
+    a.plan_T = d->plan_mask ? d->plan_tokens_per_stream : 0;
 
     hipStream_t s = static_cast<hipStream_t>(stream);
     const int grid = 8 * a.items_per_xcd;

@@ -58,10 +58,12 @@ struct StepArgs {
     int n_items;
     int items_per_xcd;          // ceil(n_items / 8)
     float qscale;               // softmax scale * log2(e)
+    int plan_T;                 // plan tokens per stream when the self-only plan mask is on, else 0
 };
 
 struct VideoInfo {
     int p0, L, e0, E;
+    int plan0;  // first prefix key of the plan segment under the self-only mask; L when off
 };
 
 __device__ inline VideoInfo video_info(const StepArgs& a, int v)
@@ -78,6 +80,7 @@ __device__ inline VideoInfo video_info(const StepArgs& a, int v)
         vi.e0 = 0;
         vi.E = a.num_events;
     }
+    vi.plan0 = a.plan_T > 0 ? vi.L - vi.E * a.plan_T : vi.L;
     return vi;
 }
 
@@ -159,6 +162,7 @@ struct UnitInfo {
     long key_off;  // element offset of its first key in k/v_prefix or k/v_event
     int nk;        // valid keys (1..64)
     int stream;    // -1 for a prefix unit, else the video-local stream whose rows see it
+    int k0;        // index of its first key in the video's prefix (prefix unit) or own cache
 };
 
 __device__ inline UnitInfo unit_info(const StepArgs& a, const VideoInfo& vi, int upre, const int* start,
@@ -170,6 +174,7 @@ __device__ inline UnitInfo unit_info(const StepArgs& a, const VideoInfo& vi, int
         ui.key_off = ((long)(vi.p0 + k0) * a.H_kv + g) * a.D;
         ui.nk = min(kUnit, vi.L - k0);
         ui.stream = -1;
+        ui.k0 = k0;
         return ui;
     }
     const int uo = u - upre;
@@ -182,7 +187,22 @@ __device__ inline UnitInfo unit_info(const StepArgs& a, const VideoInfo& vi, int
     ui.key_off = (((long)(vi.e0 + lo) * a.cap + t0) * a.H_kv + g) * a.D;
     ui.nk = min(kUnit, nlen[lo] - t0);
     ui.stream = lo;
+    ui.k0 = t0;
     return ui;
+}
+
+// Whether prefix key j of a video is hidden from the rows of its stream f.
+// The keys before the plan segment are shared.  Under the "self G-token
+// only" mask of Table 8 the segment (the last E*T prefix keys) is split into
+// E runs of T keys, run f holding stream f's global tokens, and a stream sees
+// its own run only.  With the mask off the segment starts at L, past every
+// valid key.  (Keys past the valid count are excluded separately.)  The
+// tests are combined with bitwise operators so that the compiler selects
+// rather than branches per key.
+__device__ inline bool plan_key_hidden(const StepArgs& a, const VideoInfo& vi, int j, int f)
+{
+    const int lo = vi.plan0 + f * a.plan_T;
+    return (j >= vi.plan0) & ((j < lo) | (j >= lo + a.plan_T));
 }
 
 // Global (stream, head) row of item row r (r counted from 0 within the video).

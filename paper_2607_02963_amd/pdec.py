@@ -36,7 +36,8 @@ class Dims(ctypes.Structure):
                 ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("event_cap", ctypes.c_int32), ("max_prefix_len", ctypes.c_int32),
                 ("max_events_per_video", ctypes.c_int32), ("dtype", ctypes.c_int32),
-                ("softmax_scale", ctypes.c_float), ("prefix_tokens", ctypes.c_int64)]
+                ("softmax_scale", ctypes.c_float), ("prefix_tokens", ctypes.c_int64),
+                ("plan_mask", ctypes.c_int32), ("plan_tokens_per_stream", ctypes.c_int32)]
 
 
 class PdecError(RuntimeError):
@@ -119,9 +120,10 @@ def _stream(stream, device) -> ctypes.c_void_p:
 
 
 def make_dims(num_events, H_q, H_kv, D, cap, max_prefix_len, dtype_code, scale=0.0,
-              max_events_per_video=0, prefix_tokens=0) -> Dims:
+              max_events_per_video=0, prefix_tokens=0, plan_mask=0, plan_per_stream=0) -> Dims:
     return Dims(int(num_events), int(H_q), int(H_kv), int(D), int(cap), int(max_prefix_len),
-                int(max_events_per_video), int(dtype_code), float(scale), int(prefix_tokens))
+                int(max_events_per_video), int(dtype_code), float(scale), int(prefix_tokens), int(plan_mask),
+                int(plan_per_stream))
 
 
 def workspace_size(dims: Dims, num_videos: int = 1) -> int:
@@ -155,20 +157,23 @@ def _outputs(q, out, lse, workspace, ws_bytes):
 
 
 def attn_step(q, k_prefix, v_prefix, k_event, v_event, event_lens, prefix_lens, *, out=None, lse=None,
-              workspace=None, max_prefix_len=None, scale=0.0, stream=None, want_lse=True):
+              workspace=None, max_prefix_len=None, scale=0.0, stream=None, want_lse=True, plan_mask=0,
+              plan_per_stream=0):
     """One event-parallel decode step of one video; returns (out, lse).
 
     q [E,H_q,D]; k/v_prefix [>=L,H_kv,D]; k/v_event [E,cap,H_kv,D];
     event_lens int32 [E] (n_e incl. the current token, 0 = ended);
     prefix_lens int32 [1] (device).  ``max_prefix_len`` bounds L (default:
-    the prefix tensors' row count).
+    the prefix tensors' row count).  ``plan_mask`` 1 with ``plan_per_stream``
+    T selects the "self G-token only" mask (pdec_dims in include/pdec.h).
     """
     E, H_q, D = q.shape
     H_kv = k_prefix.shape[1]
     cap = k_event.shape[1]
     if max_prefix_len is None:
         max_prefix_len = k_prefix.shape[0]
-    dims = make_dims(E, H_q, H_kv, D, cap, max_prefix_len, _dtype_code(q), scale)
+    dims = make_dims(E, H_q, H_kv, D, cap, max_prefix_len, _dtype_code(q), scale, plan_mask=plan_mask,
+                     plan_per_stream=plan_per_stream)
     ws_bytes = workspace_size(dims, 1)
     out, lse, workspace = _outputs(q, out, lse, workspace, ws_bytes)
     args = [_dev(q, "q", ndim=3), _dev(k_prefix, "k_prefix", q.dtype, 3), _dev(v_prefix, "v_prefix", q.dtype, 3),
@@ -189,7 +194,7 @@ def attn_step(q, k_prefix, v_prefix, k_event, v_event, event_lens, prefix_lens, 
 
 def attn_step_ragged(q, k_prefix, v_prefix, cu_prefix, k_event, v_event, event_lens, cu_events, *,
                      max_prefix_len, max_events_per_video, out=None, lse=None, workspace=None, scale=0.0,
-                     stream=None, want_lse=True):
+                     stream=None, want_lse=True, plan_mask=0, plan_per_stream=0):
     """One decode step over a ragged batch of videos; returns (out, lse).
 
     k/v_prefix packed [sum L_v, H_kv, D]; cu_prefix, cu_events int32 [V+1]
@@ -200,7 +205,7 @@ def attn_step_ragged(q, k_prefix, v_prefix, cu_prefix, k_event, v_event, event_l
     cap = k_event.shape[1]
     V = cu_prefix.shape[0] - 1
     dims = make_dims(SE, H_q, H_kv, D, cap, max_prefix_len, _dtype_code(q), scale, max_events_per_video,
-                     prefix_tokens=k_prefix.shape[0])
+                     prefix_tokens=k_prefix.shape[0], plan_mask=plan_mask, plan_per_stream=plan_per_stream)
     ws_bytes = workspace_size(dims, V)
     out, lse, workspace = _outputs(q, out, lse, workspace, ws_bytes)
     if cu_events.shape[0] != V + 1 or k_event.shape[0] != SE or event_lens.shape[0] != SE:

@@ -44,8 +44,9 @@ class DevStep:
         self.cu_events = dev_int(s.cu_events)
         self.prefix_lens = dev_int(s.prefix_lens[:1])
 
-    def run(self, ragged: bool | None = None, out=None, lse=None, workspace=None):
+    def run(self, ragged: bool | None = None, out=None, lse=None, workspace=None, plan_mask=0, plan_per_stream=0):
         s = self.s
+        plan = dict(plan_mask=plan_mask, plan_per_stream=plan_per_stream)
         if ragged is None:
             ragged = s.num_videos > 1
         if ragged:
@@ -53,15 +54,16 @@ class DevStep:
                                          self.v_event, self.event_lens, self.cu_events,
                                          max_prefix_len=int(s.prefix_lens.max(initial=0)),
                                          max_events_per_video=int(s.events_per_video.max()), out=out, lse=lse,
-                                         workspace=workspace, scale=s.scale)
+                                         workspace=workspace, scale=s.scale, **plan)
         assert s.num_videos == 1
         return pdec.attn_step(self.q, self.k_prefix, self.v_prefix, self.k_event, self.v_event, self.event_lens,
-                              self.prefix_lens, out=out, lse=lse, workspace=workspace, scale=s.scale)
+                              self.prefix_lens, out=out, lse=lse, workspace=workspace, scale=s.scale, **plan)
 
 
-def oracle_ref(s: wl.StepInputs, row_select=None):
+def oracle_ref(s: wl.StepInputs, row_select=None, plan_mask=0, plan_per_stream=0):
     return oracle.attn_step(s.q, s.k_prefix, s.v_prefix, s.k_event, s.v_event, s.event_lens, s.cu_prefix,
-                            s.cu_events, scale=s.scale, row_select=row_select)
+                            s.cu_events, scale=s.scale, row_select=row_select, plan_mask=plan_mask,
+                            plan_per_stream=plan_per_stream)
 
 
 def check(dtype: str, out, lse, ref_out, ref_lse, sel=None, what=""):

@@ -30,7 +30,8 @@ def _dims(**kw):
                 dtype_code=pdec.PDEC_DTYPE_BF16)
     base.update(kw)
     return pdec.make_dims(base["num_events"], base["H_q"], base["H_kv"], base["D"], base["cap"],
-                          base["max_prefix_len"], base["dtype_code"])
+                          base["max_prefix_len"], base["dtype_code"], plan_mask=base.get("plan_mask", 0),
+                          plan_per_stream=base.get("plan_per_stream", 0))
 
 
 def test_strerror_covers_codes():
@@ -45,6 +46,17 @@ def test_workspace_size_rejects_bad_dims():
     assert pdec.workspace_size(_dims(cap=0)) == 0
     assert pdec.workspace_size(_dims(dtype_code=7)) == 0
     assert pdec.workspace_size(_dims(), num_videos=0) == 0
+    assert pdec.workspace_size(_dims(plan_mask=2)) == 0    # mask modes are 0 and 1
+    assert pdec.workspace_size(_dims(plan_mask=-1)) == 0
+    assert pdec.workspace_size(_dims(plan_mask=1, plan_per_stream=-1)) == 0
+
+
+def test_self_plan_mask_leaves_the_work_split_alone():
+    """The mask changes which keys a row sees, not which keys are read."""
+    plain = _dims()
+    masked = _dims(plan_mask=1, plan_per_stream=2)
+    assert pdec.workspace_size(masked) == pdec.workspace_size(plain)
+    assert pdec.query_plan(masked) == pdec.query_plan(plain)
 
 
 def test_workspace_holds_every_partial_slot():
