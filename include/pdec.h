@@ -92,8 +92,9 @@ const char* pdec_strerror(int status);
 /*
  * Bytes of workspace a step call with these dims needs (num_videos = 1 for
  * pdec_attn_step).  The workspace holds the per-chunk partial softmax states
- * (running max, normaliser and un-normalised output per query row) that the
- * split of the prefix across compute units produces.  Returns 0 if the dims
+ * (running max and normaliser in float32, and the normalised output in the
+ * inputs' element type, per query row) that the split of the prefix across
+ * compute units produces.  Returns 0 if the dims
  * are invalid.  Pure host function: touches no device.
  */
 size_t pdec_workspace_size(const pdec_dims* dims, int32_t num_videos);

@@ -1,13 +1,15 @@
 // Finish pass: merge the chunk states of every (stream, head) row.
 //
-// Slot c holds (m_c, l_c, o_c) over a disjoint part of the row's visible
+// Slot c holds (m_c, l_c, u_c) over a disjoint part of the row's visible
 // keys (prefix units and the stream's own units, pdec_common.h): m_c a
-// reference max (base 2), l_c = sum 2^(x - m_c), o_c = sum 2^(x - m_c) v.
-// Over the union, with M = max m_c and L = sum 2^(m_c - M) l_c,
-//   out = sum 2^(m_c - M) o_c / L,   lse = ln 2 * (M + log2 L),
-// which is exactly the softmax of the row's §3.4-masked scores, regrouped.
-// A slot whose part holds none of the row's keys has l = 0 and a reference m
-// far below any score, so its weight is 0.
+// reference max (base 2), l_c = sum 2^(x - m_c), and u_c = o_c / l_c with
+// o_c = sum 2^(x - m_c) v, stored in the inputs' element type (u_c is a
+// convex combination of value rows, so it keeps their range).  Over the
+// union, with M = max m_c and L = sum 2^(m_c - M) l_c,
+//   out = sum 2^(m_c - M) l_c u_c / L,   lse = ln 2 * (M + log2 L),
+// which is the softmax of the row's §3.4-masked scores, regrouped (up to
+// the rounding of u_c).  A slot whose part holds none of the row's keys has
+// l = 0, u = 0 and a reference m far below any score, so its weight is 0.
 // A stream with n_e == 0 has ended: out row 0, lse -inf.
 //
 // One work-group of four waves per row.  A row's slots are contiguous in the
@@ -15,7 +17,7 @@
 // slot groups of D/4 lanes (4 d each); group s takes slots s, s + 4SG, ...
 // Their first NL slots are loaded before anything else, so those loads are
 // in flight while wave 0 reduces (M, L) and stores the slot weights
-// 2^(m_c - M) in LDS; the group sums then meet through lane shuffles and LDS.
+// 2^(m_c - M) l_c in LDS; the group sums then meet through lane shuffles and LDS.
 #pragma once
 
 #include "pdec_common.h"
@@ -23,6 +25,15 @@
 namespace pdec {
 
 constexpr int kMaxChunks = 512;  // slot weights held in LDS per row
+
+// Four consecutive partial-output elements as floats.
+__device__ inline float4 load_part4(const float* p) { return *reinterpret_cast<const float4*>(p); }
+__device__ inline float4 load_part4(const uint16_t* p)
+{
+    const uint2 u = *reinterpret_cast<const uint2*>(p);
+    return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u), __uint_as_float(u.y << 16),
+                       __uint_as_float(u.y & 0xffff0000u));
+}
 
 template <typename T, int D>
 __global__ __launch_bounds__(256) void finish_kernel(StepArgs a)
@@ -52,13 +63,13 @@ __global__ __launch_bounds__(256) void finish_kernel(StepArgs a)
     const int nch = min(a.video_chunks[video_of_event(a, e)], a.max_chunks);
     const int grp = wave * SG + lane / TPR;
     const int d0 = 4 * (lane % TPR);
-    const float* __restrict__ po = a.part_o + qr * a.max_chunks * D + d0;
+    const T* __restrict__ po = static_cast<const T*>(a.part_o) + qr * a.max_chunks * D + d0;
 
     float4 x[NL];
 #pragma unroll
     for (int i = 0; i < NL; ++i) {
         const int c = grp + GS * i;
-        x[i] = c < nch ? *reinterpret_cast<const float4*>(po + (long)c * D) : make_float4(0.f, 0.f, 0.f, 0.f);
+        x[i] = c < nch ? load_part4(po + (long)c * D) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
 
     if (wave == 0) {
@@ -70,9 +81,9 @@ __global__ __launch_bounds__(256) void finish_kernel(StepArgs a)
         float ls = 0.f;
         for (int c = lane; c < nch; c += 64) {
             const float2 s = ml[c];
-            const float w = fast_exp2(s.x - mx);  // 0 for a slot without keys of this row
+            const float w = fast_exp2(s.x - mx) * s.y;  // 0 for a slot without keys of this row
             wts[c] = w;
-            ls += w * s.y;
+            ls += w;
         }
 #pragma unroll
         for (int off = 32; off > 0; off >>= 1) ls += __shfl_xor(ls, off);
@@ -97,7 +108,7 @@ __global__ __launch_bounds__(256) void finish_kernel(StepArgs a)
     }
     for (int c = grp + GS * NL; c < nch; c += GS) {  // rows with more than 64 slots
         const float w = wts[c];
-        const float4 y = *reinterpret_cast<const float4*>(po + (long)c * D);
+        const float4 y = load_part4(po + (long)c * D);
         acc.x += w * y.x;
         acc.y += w * y.y;
         acc.z += w * y.z;

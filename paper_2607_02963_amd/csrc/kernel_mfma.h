@@ -427,9 +427,15 @@ __global__ __launch_bounds__(512) void split_mfma_kernel(StepArgs a)
         if (r < nrows) {
             const long qr = row_qrow(a, vi, id.g, row0 + r);
             const long slot = qr * a.max_chunks + id.c;
-            float* dst = a.part_o + slot * D;
+            // o / l in bf16: a convex combination of V rows, so in V's range
+            const float inv = l_part[nt] > 0.f ? 1.f / l_part[nt] : 0.f;
+            uint16_t* dst = static_cast<uint16_t*>(a.part_o) + slot * D;
 #pragma unroll
-            for (int dt = 0; dt < C::DT; ++dt) *reinterpret_cast<f32x4_t*>(dst + 16 * dt + 4 * lg) = o[nt][dt];
+            for (int dt = 0; dt < C::DT; ++dt) {
+                const f32x4_t v = o[nt][dt];
+                *reinterpret_cast<uint2*>(dst + 16 * dt + 4 * lg) =
+                    make_uint2(pack_bf16x2(v[0] * inv, v[1] * inv), pack_bf16x2(v[2] * inv, v[3] * inv));
+            }
             if (lg == 0) *reinterpret_cast<float2*>(a.part_ml + 2 * slot) = make_float2(m_ref[nt], l_part[nt]);
         }
     }

@@ -192,7 +192,7 @@ __device__ inline float row_softmax(float x, float& m_ref, float& l_lane, float 
 // Merge of the four waves' states of an item and the write of its slot.
 // o0, o1, o2 hold waves 1, 2, 3's outputs (RT x D floats, row-major) in LDS;
 // the lane owns d0 .. d0 + DPL - 1 when `owner`.
-template <int D, int RT, int DPL>
+template <typename T, int D, int RT, int DPL>
 __device__ inline void valu_merge_write(const StepArgs& a, const ValuItem& it, int w, int lane, bool owner, int d0,
                                         const float (&m_ref)[RT], const float (&l_lane)[RT], const float (&o)[RT][DPL],
                                         float (*m_s)[RT], float (*l_s)[RT], float* o0, float* o1, float* o2)
@@ -232,13 +232,14 @@ __device__ inline void valu_merge_write(const StepArgs& a, const ValuItem& it, i
         }
         const long qr = row_qrow(a, it.vi, it.id.g, it.row0 + r);
         const long slot = qr * a.max_chunks + it.id.c;
-        float* dst = a.part_o + slot * D + d0;
+        T* dst = static_cast<T*>(a.part_o) + slot * D + d0;
+        const float inv = L > 0.f ? 1.f / L : 0.f;  // stored normalised, in the inputs' type
 #pragma unroll
         for (int j = 0; j < DPL; ++j) {
             float acc = f[0] * o[r][j];
 #pragma unroll
             for (int x = 1; x < NW; ++x) acc += f[x] * o_other[x - 1][r * D + d0 + j];
-            dst[j] = acc;
+            dst[j] = from_f32<T>(acc * inv);
         }
         if (lane == 0) *reinterpret_cast<float2*>(a.part_ml + 2 * slot) = make_float2(M, L);
     }
@@ -432,7 +433,7 @@ __global__ __launch_bounds__(256) void split_valu_bf16_kernel(StepArgs a)
         }
     }
 
-    valu_merge_write<D, RT, DPL>(a, it, w, lane, true, lane * DPL, m_ref, l_lane, o, m_s, l_s, o_s[0], o_s[1],
+    valu_merge_write<uint16_t, D, RT, DPL>(a, it, w, lane, true, lane * DPL, m_ref, l_lane, o, m_s, l_s, o_s[0], o_s[1],
                                  o_s[2]);
 }
 
@@ -572,7 +573,7 @@ __global__ __launch_bounds__(256) void split_valu_f32_kernel(StepArgs a)
         wave_lds_sync();  // p_s is rewritten by the next unit
     }
 
-    valu_merge_write<D, RT, DPL>(a, it, w, lane, true, lane * DPL, m_ref, l_lane, o, m_s, l_s, o_s[0], o_s[1],
+    valu_merge_write<float, D, RT, DPL>(a, it, w, lane, true, lane * DPL, m_ref, l_lane, o, m_s, l_s, o_s[0], o_s[1],
                                  o_s[2]);
 }
 

@@ -50,7 +50,8 @@ struct Plan {
     int unit_per_chunk;
     int max_chunks;
     long n_items;
-    size_t part_floats; // floats of partial state
+    size_t part_o_bytes;  // normalised partial outputs
+    size_t part_ml_bytes; // (max, normaliser) pairs
     size_t ws_bytes;
 };
 
@@ -130,8 +131,10 @@ Plan make_plan(const pdec_dims* d, int num_videos)
     p.max_chunks = (int)std::max<long>(1, ceil_div(units_max, p.unit_per_chunk));
     p.n_items = (long)num_videos * d->num_kv_heads * p.max_chunks * p.rg_max;
     const size_t rows = (size_t)d->num_events * d->num_q_heads;
-    p.part_floats = (size_t)p.max_chunks * rows * ((size_t)d->head_dim + 2);
-    p.ws_bytes = p.part_floats * sizeof(float) + (size_t)num_videos * sizeof(int32_t);
+    const size_t elem = d->dtype == PDEC_DTYPE_BF16 ? 2 : 4;
+    p.part_o_bytes = (size_t)p.max_chunks * rows * d->head_dim * elem;  // a multiple of 128 bytes
+    p.part_ml_bytes = (size_t)p.max_chunks * rows * 2 * sizeof(float);
+    p.ws_bytes = p.part_o_bytes + p.part_ml_bytes + (size_t)num_videos * sizeof(int32_t);
     return p;
 }
 
@@ -213,9 +216,9 @@ int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_pr
     a.out = out;
     a.lse = lse;
     const size_t rows = (size_t)d->num_events * d->num_q_heads;
-    a.part_o = static_cast<float*>(workspace);
-    a.part_ml = a.part_o + (size_t)p.max_chunks * rows * d->head_dim;
-    a.video_chunks = reinterpret_cast<int32_t*>(a.part_o + p.part_floats);
+    a.part_o = workspace;
+    a.part_ml = reinterpret_cast<float*>(static_cast<char*>(workspace) + p.part_o_bytes);
+    a.video_chunks = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + p.part_o_bytes + p.part_ml_bytes);
     a.num_videos = num_videos;
     a.num_events = d->num_events;
     a.H_q = d->num_q_heads;

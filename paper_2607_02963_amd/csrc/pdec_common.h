@@ -12,8 +12,8 @@
 // prefix unit is read by every row; an own unit of stream f only by the
 // rows of f (other rows are masked).  Units are dealt to chunks of
 // `unit_per_chunk`; a work item (video, kv head, chunk, row group) runs its
-// units and leaves one partial softmax state (max m, normaliser l,
-// un-normalised output o) per row in slot `chunk`.  Each prefix K/V byte is
+// units and leaves one partial softmax state (max m, normaliser l, output
+// o / l in the inputs' element type) per row in slot `chunk`.  Each prefix K/V byte is
 // fetched once for all rows of the item — the point of decoding the streams
 // together — and a stream's own rows are fetched once for its G rows.
 // The finish pass merges the slots of each row.
@@ -45,7 +45,8 @@ struct StepArgs {
     const int32_t* prefix_len;  // one video: [1]; null for a ragged batch
     void* out;
     float* lse;                 // may be null
-    float* part_o;              // [SE*H_q, max_chunks, D]: un-normalised outputs
+    void* part_o;               // [SE*H_q, max_chunks, D]: outputs divided by their normaliser, in
+                                // the inputs' element type (bf16 or float32)
     float* part_ml;             // [SE*H_q, max_chunks, 2]: (reference max, normaliser)
     int32_t* video_chunks;      // [V]: chunks holding states, written by the split pass
     int num_videos;

@@ -67,7 +67,8 @@ def test_workspace_holds_every_partial_slot():
     assert chunk % 64 == 0
     units_max = 32768 // 64 + 32 * 3
     slots = -(-units_max // (chunk // 64))
-    assert pdec.workspace_size(d) == slots * 32 * 28 * (128 + 2) * 4 + 4
+    # normalised outputs in bf16, (max, normaliser) in float32, one chunk count
+    assert pdec.workspace_size(d) == slots * 32 * 28 * (128 * 2 + 2 * 4) + 4
 
 
 @pytest.mark.parametrize("E,G,dt,expect", [(32, 7, pdec.PDEC_DTYPE_BF16, pdec.PATH_MFMA),

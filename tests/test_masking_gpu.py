@@ -115,8 +115,11 @@ def test_other_videos_never_read():
 
 def test_stream_permutation_permutes_outputs():
     """Permuting streams permutes the rows.  Each stream's own rows are placed
-    by the work split after the streams before it, so the fp32 summation
-    order of a row may change with the permutation: equal to rounding."""
+    by the work split after the streams before it, so the chunks a row's keys
+    fall into, its fp32 summation order and the bf16 rounding of its stored
+    chunk outputs may change with the permutation: equal to within two bf16
+    units in the last place of the largest output (one for the output's own
+    rounding, one for the chunk outputs')."""
     s = _step()
     o1, l1 = DevStep(s).run()
     perm = np.array([5, 2, 6, 0, 3, 1, 4])
@@ -127,7 +130,9 @@ def test_stream_permutation_permutes_outputs():
     pt = torch.from_numpy(perm).cuda()
     a, b = o1[pt].float(), o2.float()
     assert torch.equal(torch.isneginf(l1[pt]), torch.isneginf(l2))
-    assert (a - b).abs().max().item() <= 2 ** -8 * max(a.abs().max().item(), 1e-3)
+    top = max(a.abs().max().item(), 1e-3)
+    ulp = 2.0 ** (np.floor(np.log2(top)) - 7)  # bf16 spacing at the largest output
+    assert (a - b).abs().max().item() <= 2 * ulp
     live = ~torch.isneginf(l2)
     assert (l1[pt][live] - l2[live]).abs().max().item() <= 1e-5
 
