@@ -64,7 +64,7 @@ __device__ inline uint32_t pack_bf16x2(float lo, float hi)
     return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));
 }
 
-// Reductions over the 4 lane groups (lanes l, l^16, l^32, l^48) that hold one
+// Reduction over the 4 lane groups (lanes l, l^16, l^32, l^48) that hold one
 // query row in the S^T accumulator layout.  v_permlane16_swap exchanges odd
 // 16-lane rows of one operand with even rows of the other, v_permlane32_swap
 // the upper half of one with the lower half of the other; with the value in
@@ -76,13 +76,6 @@ __device__ inline float max_over_groups(float x)
     const float y = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
     const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(y), __float_as_uint(y), false, false);
     return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
-}
-__device__ inline float sum_over_groups(float x)
-{
-    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    const float y = __uint_as_float(a[0]) + __uint_as_float(a[1]);
-    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(y), __float_as_uint(y), false, false);
-    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
 // Initial reference max: finite, so no -inf special cases are needed; the
@@ -220,12 +213,17 @@ __global__ __launch_bounds__(512) void split_mfma_kernel(StepArgs a)
         }
     };
 
-    f32x4_t o[NT][C::DT];
+    // The row normaliser is one more matrix product per block, ones^T P^T:
+    // its accumulator holds the row sum of the block's bf16 P (the same P
+    // that meets V) in each of a lane's four elements, in every lane group of
+    // the row, which spares the vector ALUs the sum (they bound the loop).
+    f32x4_t o[NT][C::DT], lsum[NT];
     float m_ref[NT], l_part[NT];
+    const bf16x8_t ones = as_bf16x8(u32x4_t{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u});
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
         m_ref[nt] = kMinRef;
-        l_part[nt] = 0.f;
+        lsum[nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int dt = 0; dt < C::DT; ++dt) o[nt][dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     }
@@ -309,7 +307,7 @@ __global__ __launch_bounds__(512) void split_mfma_kernel(StepArgs a)
                 const bool up = mt[nt] > m_ref[nt] + 8.f;
                 const float alpha = up ? fast_exp2(m_ref[nt] - mt[nt]) : 1.f;
                 m_ref[nt] = up ? mt[nt] : m_ref[nt];
-                l_part[nt] *= alpha;
+                lsum[nt] *= alpha;
 #pragma unroll
                 for (int dt = 0; dt < C::DT; ++dt) o[nt][dt] *= alpha;
             }
@@ -322,10 +320,10 @@ __global__ __launch_bounds__(512) void split_mfma_kernel(StepArgs a)
             for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) p[4 * kt + i] = fast_exp2(fmaf(s[kt][nt][i], c, -m_ref[nt]));
-            l_part[nt] += ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
             const u32x4_t pk = {pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]),
                                 pack_bf16x2(p[6], p[7])};
             pf[nt] = as_bf16x8(pk);
+            lsum[nt] = mfma_16x16x32(ones, pf[nt], lsum[nt]);
         }
 #pragma unroll
         for (int dt = 0; dt < C::DT; ++dt) {
@@ -376,9 +374,8 @@ __global__ __launch_bounds__(512) void split_mfma_kernel(StepArgs a)
         }
     }
 
-    // row normaliser: sum the 4 lane groups of each row
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) l_part[nt] = sum_over_groups(l_part[nt]);
+    for (int nt = 0; nt < NT; ++nt) l_part[nt] = lsum[nt][0];
 
     if constexpr (WK == 2) {
         // key group 1 hands its state to key group 0 through LDS
