@@ -12,16 +12,18 @@ INCLUDE = os.path.join(ROOT, "include")
 LIBRARY = os.path.join(PKG, "_build", "libpdec.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-# Packed fp32 ALU instructions are disabled for all device code.  The
-# kernels run with the IEEE mode bit clear and are compiled without NaN
-# semantics: no result depends on NaN propagation (masked scores are -inf,
-# reads past valid rows never happen), and the compiler then emits plain
-# v_max/v_max3 without a quieting v_max(x, x) before each operand, which
-# is about a tenth of the split kernels' vector instructions.
-HIP_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
+# Packed fp32 ALU instructions are disabled for all device code.
+HIP_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-             "-fno-honor-nans", "-mno-amdgpu-ieee",
              "-Wno-unused-command-line-argument"]
+
+# The matrix-core kernels run with the IEEE mode bit clear and are compiled
+# without NaN semantics: no result depends on NaN propagation (masked scores
+# are -inf, reads past valid rows never happen), and the compiler then emits
+# plain v_max/v_max3 without a quieting v_max(x, x) before each operand, a
+# tenth of their vector instructions.  The vector-ALU kernels compile to
+# slower code with the same flags, so they keep the defaults.
+SOURCE_FLAGS = {"split_mfma.hip": ["-fno-honor-nans", "-mno-amdgpu-ieee"]}
 
 
 def sources():
@@ -38,19 +40,33 @@ def source_digest() -> str:
             with open(os.path.join(d, f), "rb") as fh:
                 h.update(fh.read())
     h.update(" ".join(HIP_FLAGS).encode())
+    for name in sorted(SOURCE_FLAGS):
+        h.update((name + " " + " ".join(SOURCE_FLAGS[name])).encode())
     return h.hexdigest()
 
 
-def build_library(verbose: bool = False, extra_flags=()) -> str:
-    os.makedirs(os.path.dirname(LIBRARY), exist_ok=True)
-    tmp = LIBRARY + ".tmp"
-    cmd = [HIPCC, *HIP_FLAGS, *extra_flags, "-I", INCLUDE, "-I", CSRC, *sources(), "-o", tmp]
+def _run(cmd, verbose):
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("hipcc failed:\n" + " ".join(cmd) + "\n" + r.stdout + r.stderr)
     if verbose:
         print(" ".join(cmd))
         print(r.stderr)
+
+
+def build_library(verbose: bool = False, extra_flags=()) -> str:
+    """Compiles each translation unit with its flags, then links them."""
+    out_dir = os.path.dirname(LIBRARY)
+    os.makedirs(out_dir, exist_ok=True)
+    objs = []
+    for src in sources():
+        name = os.path.basename(src)
+        obj = os.path.join(out_dir, name + ".o")
+        _run([HIPCC, *HIP_FLAGS, *SOURCE_FLAGS.get(name, []), *extra_flags, "-I", INCLUDE, "-I", CSRC,
+              "-c", src, "-o", obj], verbose)
+        objs.append(obj)
+    tmp = LIBRARY + ".tmp"
+    _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp], verbose)
     os.replace(tmp, LIBRARY)
     return LIBRARY
 

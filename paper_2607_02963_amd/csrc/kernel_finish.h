@@ -15,8 +15,10 @@
 // One work-group of four waves per row.  A row's slots are contiguous in the
 // workspace ([row][slot][D] and [row][slot](m, l)).  The lanes form 4*SG
 // slot groups of D/4 lanes (4 d each); group s takes slots s, s + 4SG, ...
-// Their first NL slots are loaded before anything else, so those loads are
-// in flight while wave 0 reduces (M, L) and stores the slot weights
+// Their first NL slots are loaded before anything else (slot indices clamped
+// to the last slot, so the loads need no branch and the compiler issues them
+// together), so those loads are in flight while wave 0 reduces (M, L) and
+// stores the slot weights
 // 2^(m_c - M) l_c in LDS; the group sums then meet through lane shuffles and LDS.
 #pragma once
 
@@ -69,7 +71,7 @@ __global__ __launch_bounds__(256) void finish_kernel(StepArgs a)
 #pragma unroll
     for (int i = 0; i < NL; ++i) {
         const int c = grp + GS * i;
-        x[i] = c < nch ? load_part4(po + (long)c * D) : make_float4(0.f, 0.f, 0.f, 0.f);
+        x[i] = load_part4(po + (long)min(c, nch - 1) * D);  // unconditional: all loads in flight at once
     }
 
     if (wave == 0) {

@@ -22,7 +22,6 @@
 
 #include "kernel_append.h"
 #include "kernel_finish.h"
-#include "kernel_mfma.h"
 #include "kernel_valu.h"
 
 namespace {
@@ -144,25 +143,8 @@ int launch_status()
     return e == hipSuccess ? PDEC_OK : PDEC_ERR_HIP;
 }
 
-template <int D, bool PLAN>
-void launch_mfma_shape(const StepArgs& a, int shape, int grid, hipStream_t s)
-{
-    switch (shape) {
-    case 1: hipLaunchKernelGGL((split_mfma_kernel<D, 1, 4, 2, PLAN>), dim3(grid), dim3(512), 0, s, a); break;
-    case 2: hipLaunchKernelGGL((split_mfma_kernel<D, 2, 4, 2, PLAN>), dim3(grid), dim3(512), 0, s, a); break;
-    default: hipLaunchKernelGGL((split_mfma_kernel<D, 2, 8, 1, PLAN>), dim3(grid), dim3(512), 0, s, a); break;
-    }
-}
-
 // The self-only plan mask has kernels of its own, so that the full design's
 // inner loop carries none of its tests.
-template <int D>
-void launch_mfma(const StepArgs& a, int shape, int grid, hipStream_t s)
-{
-    if (a.plan_T > 0) launch_mfma_shape<D, true>(a, shape, grid, s);
-    else launch_mfma_shape<D, false>(a, shape, grid, s);
-}
-
 template <typename T, int D, bool PLAN>
 void launch_valu_kernel(const StepArgs& a, int grid, hipStream_t s)
 {
@@ -244,8 +226,7 @@ int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_pr
     if (timer_slot >= 0 && hipEventRecord(static_cast<hipEvent_t>(g_timer_start[timer_slot]), s) != hipSuccess)
         return PDEC_ERR_HIP;
     if (p.path == kPathMfma) {
-        if (d->head_dim == 128) launch_mfma<128>(a, p.shape, grid, s);
-        else launch_mfma<64>(a, p.shape, grid, s);
+        launch_split_mfma(a, p.shape, grid, s);
     } else if (bf16) {
         if (d->head_dim == 128) launch_valu<uint16_t, 128>(a, grid, s);
         else launch_valu<uint16_t, 64>(a, grid, s);

@@ -62,6 +62,9 @@ struct StepArgs {
     int plan_T;                 // plan tokens per stream when the self-only plan mask is on, else 0
 };
 
+// Launch of the matrix-core split pass (its own translation unit).
+void launch_split_mfma(const StepArgs& a, int shape, int grid, hipStream_t stream);
+
 struct VideoInfo {
     int p0, L, e0, E;
     int plan0;  // first prefix key of the plan segment under the self-only mask; L when off

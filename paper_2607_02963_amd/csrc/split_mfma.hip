@@ -1,0 +1,42 @@
+// Launches of the matrix-core split kernels (kernel_mfma.h).  This
+// translation unit is compiled on its own, with the IEEE mode bit clear and
+// without NaN semantics (see the build script): the compiler then drops the
+// quieting v_max(x, x) it otherwise puts before every operand of the
+// softmax's maxima, which matters in the vector-ALU-bound block loop.  The
+// vector-ALU kernels, whose code the same flags make slower, stay in
+// pdec_api.hip.
+#include <hip/hip_runtime.h>
+
+#include "kernel_mfma.h"
+
+namespace pdec {
+
+namespace {
+
+template <int D, bool PLAN>
+void launch_shape(const StepArgs& a, int shape, int grid, hipStream_t s)
+{
+    switch (shape) {
+    case 1: hipLaunchKernelGGL((split_mfma_kernel<D, 1, 4, 2, PLAN>), dim3(grid), dim3(512), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((split_mfma_kernel<D, 2, 4, 2, PLAN>), dim3(grid), dim3(512), 0, s, a); break;
+    default: hipLaunchKernelGGL((split_mfma_kernel<D, 2, 8, 1, PLAN>), dim3(grid), dim3(512), 0, s, a); break;
+    }
+}
+
+}  // namespace
+
+// The self-only plan mask has kernels of its own, so that the full design's
+// inner loop carries none of its tests.
+void launch_split_mfma(const StepArgs& a, int shape, int grid, hipStream_t stream)
+{
+    const bool plan = a.plan_T > 0;
+    if (a.D == 128) {
+        if (plan) launch_shape<128, true>(a, shape, grid, stream);
+        else launch_shape<128, false>(a, shape, grid, stream);
+    } else {
+        if (plan) launch_shape<64, true>(a, shape, grid, stream);
+        else launch_shape<64, false>(a, shape, grid, stream);
+    }
+}
+
+}  // namespace pdec
