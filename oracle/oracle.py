@@ -64,6 +64,10 @@ def _load():
             fn.restype = ctypes.c_int
             fn.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
                            ctypes.c_void_p]
+            fn = getattr(lib, f"oracle_rope_append_{sfx}")
+            fn.restype = ctypes.c_int
+            fn.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p] + [ctypes.c_int] * 4 + \
+                [ctypes.c_double, ctypes.c_int] + [ctypes.c_void_p] * 7
             getattr(lib, f"oracle_max_threads_{sfx}").restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -169,3 +173,41 @@ def build_mask(L: int, E: int, cap: int, n, plan_mask: int = 0, plan_per_stream:
 
 def max_threads() -> int:
     return int(_load().oracle_max_threads_f64())
+
+
+def rope_append(q, k_new, event_lens, live, cu_events=None, pos_base=None, cap=None, theta=10000.0,
+                precision: str = "f64"):
+    """Rotary embedding at the shared step position plus the append's count
+    update (``oracle_rope_append`` in pdec_oracle.c).
+
+    q [SE,H_q,D], k_new [SE,H_kv,D] (float32 or bf16 bits); event_lens, live
+    [SE]; cu_events [V+1] (default one video); pos_base [V] (default 0);
+    cap the cache rows per stream (default unlimited).  Returns (q_rot,
+    k_rot, new_lens): rotated rows in the oracle precision, NaN for rows not
+    rotated this step.
+    """
+    lib = _load()
+    real = np.float64 if precision == "f64" else np.float32
+    fn = getattr(lib, f"oracle_rope_append_{precision}")
+    q, k_new = _c(q), _c(k_new)
+    dt = _dtype_code(q)
+    if _dtype_code(k_new) != dt:
+        raise TypeError("q and k_new must share one dtype")
+    SE, H_q, D = q.shape
+    H_kv = k_new.shape[1]
+    if cu_events is None:
+        cu_events = np.array([0, SE], np.int32)
+    cu_events = _c(cu_events, np.int32)
+    V = cu_events.shape[0] - 1
+    pos_base = _c(np.zeros(V, np.int32) if pos_base is None else pos_base, np.int32)
+    event_lens = _c(event_lens, np.int32)
+    live = _c(live, np.int32)
+    cap = int(cap) if cap is not None else int(2 ** 30)
+    q_rot = np.empty((SE, H_q, D), real)
+    k_rot = np.empty((SE, H_kv, D), real)
+    new_lens = np.empty(SE, np.int32)
+    rc = fn(V, _ptr(cu_events), _ptr(pos_base), H_q, H_kv, D, cap, float(theta), dt, _ptr(q), _ptr(k_new),
+            _ptr(event_lens), _ptr(live), _ptr(q_rot), _ptr(k_rot), _ptr(new_lens))
+    if rc != 0:
+        raise ValueError("oracle_rope_append rejected its arguments")
+    return q_rot, k_rot, new_lens

@@ -35,6 +35,9 @@
  *     tokens are: the plan segment is taken as the last E*T prefix tokens,
  *     stream f's tokens being the f-th run of T of them (T tokens per
  *     stream, in stream order).
+ *   - the rotary embedding at the shared step position (oracle_rope_append)
+ *     is taken in the rotate-half form with frequencies theta^(-2i/D); a
+ *     stream writing cache row t of video v stands at pos_base[v] + t.
  *
  * Arithmetic type: `real`, double by default.  The same source compiled with
  * -DORACLE_REAL=float gives the fp32 variant (functions suffixed _f32), used
@@ -65,6 +68,9 @@ typedef ORACLE_REAL real;
 /* exp / log in the arithmetic type itself (float variant must not promote). */
 static real r_exp(real x) { return sizeof(real) == sizeof(float) ? (real)expf((float)x) : (real)exp((double)x); }
 static real r_log(real x) { return sizeof(real) == sizeof(float) ? (real)logf((float)x) : (real)log((double)x); }
+static real r_cos(real x) { return sizeof(real) == sizeof(float) ? (real)cosf((float)x) : (real)cos((double)x); }
+static real r_sin(real x) { return sizeof(real) == sizeof(float) ? (real)sinf((float)x) : (real)sin((double)x); }
+static real r_pow(real x, real y) { return sizeof(real) == sizeof(float) ? (real)powf((float)x, (float)y) : (real)pow((double)x, (double)y); }
 
 /* Element `idx` of a tensor stored as float32 (dtype 0) or bfloat16 (dtype 1). */
 static real load_elem(const void* base, size_t idx, int dtype)
@@ -280,6 +286,77 @@ int ORACLE_FN(oracle_decode_loop)(int steps, int E, int H_q, int H_kv, int D, in
     free(vc);
     free(n);
     return rc;
+}
+
+/*
+ * Rotary position embedding at the shared decode position, with the cache
+ * append it precedes (§3.4: tokens of all streams at one decoding step
+ * carry one position index, so one rotation serves every stream of a
+ * video at that step).
+ *
+ * Readings (the paper fixes the shared index, not the rotation, which is
+ * its base model's):
+ *   - rotate-half form: coordinate i of a head pairs with i + D/2 and turns
+ *     by the angle pos * theta^(-2i/D), i < D/2:
+ *       y[i]       = x[i] cos a - x[i + D/2] sin a
+ *       y[i + D/2] = x[i + D/2] cos a + x[i] sin a
+ *   - a stream of video v that writes its cache row t stands at position
+ *     pos_base[v] + t; the live streams of a video step together, so they
+ *     share it.
+ *
+ * For every stream e with live[e] != 0 and t = event_lens[e] < cap:
+ *   q_rot[e, h] = R(pos) q[e, h] for every query head,
+ *   k_rot[e, g] = R(pos) k_new[e, g] for every kv head,
+ *   new_lens[e] = t + 1   (cache row t receives k_rot and v_new).
+ * A stream with live[e] == 0 ends: new_lens[e] = 0, nothing rotated.  A live
+ * stream whose cache is full keeps its count and is not rotated.  Rows not
+ * rotated are left NaN in q_rot / k_rot.
+ *   cu_events [V + 1]; pos_base [V]; q [SE, H_q, D]; k_new [SE, H_kv, D];
+ *   q_rot [SE, H_q, D], k_rot [SE, H_kv, D] (real); lens in/out [SE].
+ */
+static void rotate_head(const void* x, size_t base, int D, int dtype, real pos, real theta, real* y)
+{
+    const int half = D / 2;
+    for (int i = 0; i < half; ++i) {
+        const real a = pos * r_pow(theta, -(real)(2 * i) / (real)D);
+        const real c = r_cos(a), s = r_sin(a);
+        const real x1 = load_elem(x, base + i, dtype);
+        const real x2 = load_elem(x, base + i + half, dtype);
+        y[i] = x1 * c - x2 * s;
+        y[i + half] = x2 * c + x1 * s;
+    }
+}
+
+int ORACLE_FN(oracle_rope_append)(int V, const int32_t* cu_events, const int32_t* pos_base, int H_q, int H_kv,
+                                  int D, int cap, double theta, int dtype, const void* q, const void* k_new,
+                                  const int32_t* event_lens, const int32_t* live, real* q_rot, real* k_rot,
+                                  int32_t* new_lens)
+{
+    if (V < 1 || D < 2 || D % 2 != 0 || cap < 1 || !(theta > 0.0)) return -1;
+    const int SE = cu_events[V];
+    for (size_t i = 0; i < (size_t)SE * H_q * D; ++i) q_rot[i] = (real)NAN;
+    for (size_t i = 0; i < (size_t)SE * H_kv * D; ++i) k_rot[i] = (real)NAN;
+    for (int v = 0; v < V; ++v) {
+        for (int e = cu_events[v]; e < cu_events[v + 1]; ++e) {
+            const int t = event_lens[e];
+            if (!live[e]) {
+                new_lens[e] = 0;
+                continue;
+            }
+            if (t < 0 || t >= cap) {
+                new_lens[e] = t;
+                continue;
+            }
+            const real pos = (real)pos_base[v] + (real)t;
+            for (int h = 0; h < H_q; ++h)
+                rotate_head(q, ((size_t)e * H_q + h) * D, D, dtype, pos, (real)theta, q_rot + ((size_t)e * H_q + h) * D);
+            for (int g = 0; g < H_kv; ++g)
+                rotate_head(k_new, ((size_t)e * H_kv + g) * D, D, dtype, pos, (real)theta,
+                            k_rot + ((size_t)e * H_kv + g) * D);
+            new_lens[e] = t + 1;
+        }
+    }
+    return 0;
 }
 
 /* Threads OpenMP will use for a parallel region (1 without OpenMP). */

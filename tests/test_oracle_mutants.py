@@ -31,6 +31,11 @@ MUTANTS = {
     "plan_group_modulo": ("row[j] = (j - plan0) / plan_T == e;", "row[j] = (j - plan0) % E == e;"),
     "plan_start_off_by_one": ("(long)L - (long)E * plan_T : (long)L;", "(long)L - (long)E * plan_T + 1 : (long)L;"),
     "plan_mask_ignored": ("for (long j = plan0; j < L; ++j)", "for (long j = L; j < L; ++j)"),
+    "rope_direction": ("y[i] = x1 * c - x2 * s;", "y[i] = x1 * c + x2 * s;"),
+    "rope_frequency_exponent": ("-(real)(2 * i) / (real)D", "-(real)(i) / (real)D"),
+    "rope_pair_partner": ("load_elem(x, base + i + half, dtype);", "load_elem(x, base + (i ^ 1), dtype);"),
+    "rope_position_off_by_one": ("(real)pos_base[v] + (real)t;", "(real)pos_base[v] + (real)t + 1;"),
+    "rope_ended_keeps_count": ("new_lens[e] = 0;", "new_lens[e] = t;"),
 }
 
 

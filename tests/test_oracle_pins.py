@@ -504,3 +504,126 @@ def test_sequential_comparator_is_causal_decode():
         ro, rl = _sdpa_last_row(_f64(sq.q_steps[s, 0]), _f64(seq_k), _f64(seq_v))
         np.testing.assert_allclose(out[s, 0], ro, atol=1e-12)
         np.testing.assert_allclose(lse[s, 0], rl, atol=1e-12)
+
+
+# ---- rotary embedding at the shared step position (with the append) ----
+
+def _golden_rope():
+    cases = []
+    with open(os.path.join(GOLDEN, "rope_convention.txt")) as fh:
+        for line in fh:
+            line = line.split("#", 1)[0].strip()
+            if not line:
+                continue
+            head, tail = line.split("|")
+            D, theta, pos_base, t, c = head.split()
+            vals = tail.split()
+            cases.append(dict(D=int(D), theta=float(theta), pos_base=int(pos_base), t=int(t), c=int(c),
+                              want={int(vals[i]): float(vals[i + 1]) for i in range(0, len(vals), 2)}))
+    return cases
+
+
+@pytest.mark.parametrize("case", _golden_rope(), ids=lambda c: f"D{c['D']}p{c['pos_base']}t{c['t']}c{c['c']}")
+def test_rope_convention_matches_hand_written_table(case):
+    """Unit vectors land where the rotate-half reading with frequency
+    theta^(-2i/D) puts them, at position pos_base + t."""
+    D = case["D"]
+    x = np.zeros((1, 1, D), np.float32)
+    x[0, 0, case["c"]] = 1.0
+    q_rot, k_rot, lens = oracle.rope_append(x, x.copy(), [case["t"]], [1], pos_base=[case["pos_base"]],
+                                            theta=case["theta"])
+    want = np.zeros(D)
+    for i, v in case["want"].items():
+        want[i] = v
+    np.testing.assert_allclose(q_rot[0, 0], want, atol=1e-13)
+    np.testing.assert_allclose(k_rot[0, 0], want, atol=1e-13)
+    assert lens[0] == case["t"] + 1
+
+
+def _rope_inputs(seed, SE=5, H_q=6, H_kv=2, D=16, dtype="f32"):
+    rng = np.random.default_rng(seed)
+    q = rng.standard_normal((SE, H_q, D)).astype(np.float32)
+    k = rng.standard_normal((SE, H_kv, D)).astype(np.float32)
+    if dtype == "bf16":
+        return wl.bf16_bits(q), wl.bf16_bits(k)
+    return q, k
+
+
+def test_rope_is_complex_multiplication():
+    """Pair (x_i, x_{i+D/2}) as x_i + j x_{i+D/2} turns into z e^{j a}
+    (numpy's complex arithmetic), a = pos * theta^(-2i/D)."""
+    q, k = _rope_inputs(1)
+    lens = np.array([0, 3, 17, 250, 9], np.int32)
+    q_rot, k_rot, _ = oracle.rope_append(q, k, lens, [1] * 5, pos_base=[1000], theta=10000.0)
+    D = q.shape[-1]
+    h = D // 2
+    freq = 10000.0 ** (-np.arange(h) * 2.0 / D)
+    for e in range(5):
+        a = (1000 + lens[e]) * freq
+        for x, y in ((q[e], q_rot[e]), (k[e], k_rot[e])):
+            z = (x[:, :h].astype(np.float64) + 1j * x[:, h:].astype(np.float64)) * np.exp(1j * a)
+            np.testing.assert_allclose(y[:, :h], z.real, atol=1e-12)
+            np.testing.assert_allclose(y[:, h:], z.imag, atol=1e-12)
+
+
+def test_rope_preserves_norms_and_relative_position():
+    """A rotation keeps each pair's length, and <R(p)q, R(p')k> depends only
+    on p - p': shifting both positions by the same amount changes nothing."""
+    q, k = _rope_inputs(2, SE=1, H_q=1, H_kv=1, D=32)
+    h = 16
+
+    def rot(v, pos):  # v rotated at absolute position pos
+        r, _, _ = oracle.rope_append(v[None, None], v[None, None], [0], [1], pos_base=[pos])
+        return r[0, 0]
+
+    x = q[0, 0].astype(np.float64)
+    y = rot(q[0, 0], 25)
+    np.testing.assert_allclose(x[:h] ** 2 + x[h:] ** 2, y[:h] ** 2 + y[h:] ** 2, rtol=1e-12)
+    d1 = float(np.dot(rot(q[0, 0], 25), rot(k[0, 0], 20)))
+    d2 = float(np.dot(rot(q[0, 0], 336), rot(k[0, 0], 331)))
+    d3 = float(np.dot(rot(q[0, 0], 25), rot(k[0, 0], 9)))
+    assert abs(d1 - d2) < 1e-9 * max(1.0, abs(d1))
+    assert abs(d3 - d1) > 1e-6  # a different gap gives a different product
+
+
+def test_rope_at_position_zero_is_the_identity():
+    q, k = _rope_inputs(3)
+    q_rot, k_rot, lens = oracle.rope_append(q, k, np.zeros(5, np.int32), [1] * 5, pos_base=[0])
+    assert np.array_equal(q_rot, q.astype(np.float64)) and np.array_equal(k_rot, k.astype(np.float64))
+    assert lens.tolist() == [1] * 5
+
+
+def test_rope_streams_at_one_step_share_the_rotation():
+    """Live streams of one video at the same row share the position (§3.4);
+    another video is at its own base position."""
+    q, k = _rope_inputs(4, SE=4)
+    q[:] = q[0]
+    lens = np.array([6, 6, 6, 6], np.int32)
+    q_rot, _, _ = oracle.rope_append(q, k, lens, [1] * 4, cu_events=[0, 2, 4], pos_base=[100, 100])
+    assert np.array_equal(q_rot[0], q_rot[1]) and np.array_equal(q_rot[0], q_rot[3])
+    q_rot2, _, _ = oracle.rope_append(q, k, lens, [1] * 4, cu_events=[0, 2, 4], pos_base=[100, 50])
+    assert np.array_equal(q_rot2[0], q_rot[0]) and not np.allclose(q_rot2[2], q_rot[2])
+    # a video at base 50 row 6 equals one at base 0 row 56
+    q_rot3, _, _ = oracle.rope_append(q[2:3], k[2:3], [56], [1], pos_base=[0])
+    np.testing.assert_allclose(q_rot3[0], q_rot2[2], atol=1e-12)
+
+
+def test_rope_append_counts():
+    """Live streams advance, ended ones drop to 0, full caches stay as they
+    are and are not rotated."""
+    q, k = _rope_inputs(5)
+    lens = np.array([0, 4, 7, 3, 8], np.int32)
+    live = np.array([1, 1, 0, 1, 1], np.int32)
+    q_rot, k_rot, new = oracle.rope_append(q, k, lens, live, cap=8)
+    assert new.tolist() == [1, 5, 0, 4, 8]
+    assert np.isnan(q_rot[2]).all() and np.isnan(k_rot[4]).all()
+    assert not np.isnan(q_rot[[0, 1, 3]]).any()
+
+
+def test_rope_bf16_inputs_are_widened_exactly():
+    qb, kb = _rope_inputs(6, dtype="bf16")
+    qf, kf = wl.bf16_widen(qb), wl.bf16_widen(kb)
+    lens = np.arange(5, dtype=np.int32)
+    a = oracle.rope_append(qb, kb, lens, [1] * 5, pos_base=[77])
+    b = oracle.rope_append(qf, kf, lens, [1] * 5, pos_base=[77])
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
