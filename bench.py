@@ -181,12 +181,79 @@ def run_loop(args, torch, pdec, wl):
     print(json.dumps(rec), flush=True)
 
 
+def run_rope(args, torch, pdec, wl):
+    """The rotary embedding at the shared step position fused with the
+    append (pdec_rope_kv_append), at the 32k workload's stream shapes: 32
+    streams, H_q 28, H_kv 4, D 128, bf16, caches of 129 rows plus room for
+    the timed calls, base position 32768.  Each call rotates q in place and
+    writes one rotated key row and one value row per stream.  The K calls
+    are captured in one HIP graph (the kernel sets no memory with
+    hipMemsetAsync), so the timing is the GPU's, not the Python binding's:
+    µs per call from HIP events around a replay.  The kernel's algorithmic
+    bytes are q read and written, k_new and v_new read, the two cache rows
+    written and the counts."""
+    s = wl.long_32k()
+    E, H_q, H_kv, D = s.num_events, s.H_q, s.H_kv, s.D
+    cap = s.cap + args.warmup + 2 * args.steps + 4
+    rng = np.random.default_rng(s.seed)
+
+    def f(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+
+    q = f(s.q)
+    kn = f(wl.bf16_bits(0.5 * rng.standard_normal((E, H_kv, D)).astype(np.float32)))
+    vn = f(wl.bf16_bits(0.5 * rng.standard_normal((E, H_kv, D)).astype(np.float32)))
+    kc = torch.zeros((E, cap, H_kv, D), dtype=torch.bfloat16, device="cuda")
+    vc = torch.zeros_like(kc)
+    lens = torch.from_numpy(np.asarray(s.event_lens, np.int32)).cuda()
+    pos = torch.tensor([int(s.prefix_lens[0])], dtype=torch.int32, device="cuda")
+    live = torch.ones(E, dtype=torch.int32, device="cuda")
+
+    def call():
+        pdec.rope_kv_append(q, kn, vn, kc, vc, lens, pos, live=live)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for _ in range(args.warmup):
+            call()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for _ in range(args.steps):
+            call()
+    graph.replay()  # first replay uploads the graph
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    graph.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) / args.steps * 1e3
+    nbytes = 2 * E * H_q * D * 2 + 2 * E * H_kv * D * 2 + 2 * E * H_kv * D * 2 + 2 * E * 4
+    gbps = nbytes / (us * 1e-6) / 1e9
+    _log(f"bench: rotary append {us:.2f} us/call, {nbytes / 1e3:.1f} KB")
+    rec = {
+        "metric": "us per fused rotary embedding + cache append (shared step position), 32 streams",
+        "value": round(us, 3), "unit": "us/call", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "higher_is_better": False, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "rope_append_E32", "streams": E, "H_q": H_q, "H_kv": H_kv, "head_dim": D,
+                   "position": int(s.prefix_lens[0])},
+        "roofline": {"bound": "hbm", "achieved": round(gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(gbps / HBM_PEAK_GBPS, 5), "traffic": None,
+                     "kernel": "rope_append_kernel", "kernel_us": round(us, 3), "kernel_algorithmic_bytes": nbytes},
+    }
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="long_32k", help="long_32k | single_8k | ragged_16 | tiny_f32 | loop_64")
+    ap.add_argument("--workload", default="long_32k",
+                    help="long_32k | single_8k | ragged_16 | tiny_f32 | loop_64 | rope_append")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--plan-mask", choices=("full", "self"), default="full",
                     help="full: every stream sees all plan tokens (the full design); self: each stream sees only "
@@ -219,6 +286,9 @@ def main():
     torch.cuda.set_device(0)
     if args.workload == "loop_64":
         run_loop(args, torch, pdec, wl)
+        return
+    if args.workload == "rope_append":
+        run_rope(args, torch, pdec, wl)
         return
     s = wl.STEP_WORKLOADS[args.workload]()
     ragged = s.num_videos > 1

@@ -152,6 +152,33 @@ int pdec_kv_append(const pdec_dims* dims, const void* k_new, const void* v_new, 
                    void* v_event, int32_t* event_lens, const int32_t* live, void* stream);
 
 /*
+ * The append fused with the rotary position embedding at the shared decode
+ * position (§3.4: the tokens of all streams at one decoding step carry one
+ * position index).  For every stream e with live[e] != 0 (or every stream
+ * when live is NULL) whose cache has room, n = event_lens[e] < event_cap:
+ *   pos = pos_base[v] + n, v the stream's video;
+ *   q[e, h] is rotated by R(pos) in place, for every query head;
+ *   cache row n of k_event receives R(pos) k_new[e], of v_event v_new[e];
+ *   event_lens[e] becomes n + 1.
+ * A stream with live[e] == 0 gets event_lens[e] = 0 and nothing else; a live
+ * stream with a full cache is left unchanged, its q included.
+ * R(pos) turns coordinates (i, i + D/2) of a head by pos * rope_theta^(-2i/D),
+ * i < D/2 (the rotate-half form: y_i = x_i cos - x_{i+D/2} sin,
+ * y_{i+D/2} = x_{i+D/2} cos + x_i sin).  Angles and products are computed in
+ * double and rounded once to the element type (nearest even).
+ *   q [E, H_q, D] read and written;  k_new, v_new [E, H_kv, D];
+ *   k_event, v_event [E, event_cap, H_kv, D];  event_lens [E] read and written;
+ *   live [E] int32 or NULL;  cu_events [num_videos + 1] int32 (streams of
+ *   video v are [cu_events[v], cu_events[v+1])) or NULL for one video;
+ *   pos_base [num_videos] int32;  all device.  rope_theta > 0, finite.
+ * E = dims->num_events.  Returns a pdec_status.
+ */
+int pdec_rope_kv_append(const pdec_dims* dims, int32_t num_videos, void* q, const void* k_new,
+                        const void* v_new, void* k_event, void* v_event, int32_t* event_lens,
+                        const int32_t* live, const int32_t* cu_events, const int32_t* pos_base,
+                        float rope_theta, void* stream);
+
+/*
  * Kernel-path selection for the shared-prefix pass, for tests and tuning:
  * 0 = automatic (bfloat16 with >= 16 query rows per key/value head uses the
  * matrix-core kernel, everything else the vector kernel), 1 = always the

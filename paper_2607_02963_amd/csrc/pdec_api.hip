@@ -22,6 +22,7 @@
 
 #include "kernel_append.h"
 #include "kernel_finish.h"
+#include "kernel_rope.h"
 #include "kernel_valu.h"
 
 namespace {
@@ -315,6 +316,48 @@ int pdec_kv_append(const pdec_dims* dims, const void* k_new, const void* v_new, 
         hipLaunchKernelGGL((append_kernel<uint16_t>), dim3(a.num_events), dim3(256), 0, s, a);
     else
         hipLaunchKernelGGL((append_kernel<float>), dim3(a.num_events), dim3(256), 0, s, a);
+    return launch_status();
+}
+
+int pdec_rope_kv_append(const pdec_dims* dims, int32_t num_videos, void* q, const void* k_new, const void* v_new,
+                        void* k_event, void* v_event, int32_t* event_lens, const int32_t* live,
+                        const int32_t* cu_events, const int32_t* pos_base, float rope_theta, void* stream)
+{
+    const int rc = validate_dims(dims, num_videos);
+    if (rc != PDEC_OK) return rc;
+    if (!(rope_theta > 0.f) || !std::isfinite(rope_theta)) return PDEC_ERR_INVALID_ARG;
+    if (num_videos > 1 && !cu_events) return PDEC_ERR_INVALID_ARG;
+    const void* ptrs[] = {q, k_new, v_new, k_event, v_event};
+    for (const void* p : ptrs)
+        if (!p || !aligned16(p)) return PDEC_ERR_INVALID_ARG;
+    if (!event_lens || !aligned4(event_lens) || !pos_base || !aligned4(pos_base)) return PDEC_ERR_INVALID_ARG;
+    if ((live && !aligned4(live)) || (cu_events && !aligned4(cu_events))) return PDEC_ERR_INVALID_ARG;
+    RopeArgs a{};
+    a.q = q;
+    a.k_new = k_new;
+    a.v_new = v_new;
+    a.k_event = k_event;
+    a.v_event = v_event;
+    a.event_lens = event_lens;
+    a.live = live;
+    a.cu_events = cu_events;
+    a.pos_base = pos_base;
+    a.num_events = dims->num_events;
+    a.num_videos = num_videos;
+    a.H_q = dims->num_q_heads;
+    a.H_kv = dims->num_kv_heads;
+    a.D = dims->head_dim;
+    a.cap = dims->event_cap;
+    a.log2_theta = std::log2((double)rope_theta);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const bool bf16 = dims->dtype == PDEC_DTYPE_BF16;
+    if (a.D == 128) {
+        if (bf16) hipLaunchKernelGGL((rope_append_kernel<uint16_t, 128>), dim3(a.num_events), dim3(256), 0, s, a);
+        else hipLaunchKernelGGL((rope_append_kernel<float, 128>), dim3(a.num_events), dim3(256), 0, s, a);
+    } else {
+        if (bf16) hipLaunchKernelGGL((rope_append_kernel<uint16_t, 64>), dim3(a.num_events), dim3(256), 0, s, a);
+        else hipLaunchKernelGGL((rope_append_kernel<float, 64>), dim3(a.num_events), dim3(256), 0, s, a);
+    }
     return launch_status();
 }
 

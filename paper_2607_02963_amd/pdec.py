@@ -26,7 +26,8 @@ PDEC_DTYPE_BF16 = 1
 PATH_AUTO, PATH_VALU, PATH_MFMA = 0, 1, 2
 
 EXPORTED = ("pdec_strerror", "pdec_workspace_size", "pdec_attn_step", "pdec_attn_step_ragged",
-            "pdec_kv_append", "pdec_set_path", "pdec_query_plan", "pdec_set_split_timer")
+            "pdec_kv_append", "pdec_rope_kv_append", "pdec_set_path", "pdec_query_plan",
+            "pdec_set_split_timer")
 
 
 class Dims(ctypes.Structure):
@@ -73,6 +74,8 @@ def lib():
         L.pdec_attn_step_ragged.argtypes = [dp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         L.pdec_kv_append.restype = ctypes.c_int
         L.pdec_kv_append.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp]
+        L.pdec_rope_kv_append.restype = ctypes.c_int
+        L.pdec_rope_kv_append.argtypes = [dp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_float, vp]
         L.pdec_set_path.restype = ctypes.c_int
         L.pdec_set_path.argtypes = [ctypes.c_int]
         L.pdec_query_plan.restype = ctypes.c_int
@@ -238,6 +241,32 @@ def kv_append(k_new, v_new, k_event, v_event, event_lens, live=None, *, stream=N
             _dev(event_lens, "event_lens", torch.int32, 1),
             None if live is None else _dev(live, "live", torch.int32, 1), _stream(stream, k_new.device)]
     _check("pdec_kv_append", lib().pdec_kv_append(ctypes.byref(dims), *args))
+
+
+def rope_kv_append(q, k_new, v_new, k_event, v_event, event_lens, pos_base, live=None, cu_events=None, *,
+                   theta=10000.0, stream=None):
+    """Rotate q in place and append the rotated k and v of every live stream
+    at its shared step position (``pdec_rope_kv_append`` in include/pdec.h).
+
+    q [SE,H_q,D]; k_new/v_new [SE,H_kv,D]; k/v_event [SE,cap,H_kv,D];
+    event_lens int32 [SE] (updated); pos_base int32 [V]; live int32 [SE] or
+    None; cu_events int32 [V+1] or None for one video.
+    """
+    SE, cap, H_kv, D = k_event.shape
+    H_q = q.shape[1]
+    V = 1 if cu_events is None else cu_events.shape[0] - 1
+    dims = make_dims(SE, H_q, H_kv, D, cap, 0, _dtype_code(q), max_events_per_video=SE if V > 1 else 0)
+    if q.shape != (SE, H_q, D) or k_new.shape != (SE, H_kv, D) or v_new.shape != k_new.shape or \
+            v_event.shape != k_event.shape or pos_base.shape != (V,):
+        raise ValueError("inconsistent rotary append shapes")
+    args = [_dev(q, "q", None, 3), _dev(k_new, "k_new", q.dtype, 3), _dev(v_new, "v_new", q.dtype, 3),
+            _dev(k_event, "k_event", q.dtype, 4), _dev(v_event, "v_event", q.dtype, 4),
+            _dev(event_lens, "event_lens", torch.int32, 1),
+            None if live is None else _dev(live, "live", torch.int32, 1),
+            None if cu_events is None else _dev(cu_events, "cu_events", torch.int32, 1),
+            _dev(pos_base, "pos_base", torch.int32, 1)]
+    _check("pdec_rope_kv_append", lib().pdec_rope_kv_append(ctypes.byref(dims), V, *args, float(theta),
+                                                            _stream(stream, q.device)))
 
 
 class SplitTimer:
