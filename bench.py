@@ -247,13 +247,64 @@ def run_rope(args, torch, pdec, wl):
     print(json.dumps(rec), flush=True)
 
 
+def run_grounding(args, torch, pdec, wl):
+    """Segment-level similarity grounding over the 32k prefix's audio-visual
+    tokens (32704 tokens of width 256 after the projection, 128 time
+    segments, 32 event tokens; pdec_segment_grounding, threshold 0.5).
+    Inputs rotate over copies totalling >= 512 MB so the 256 MB MALL cannot
+    hold them.  µs per call from HIP events around K back-to-back calls; the
+    partial-pass kernel's algorithmic bytes are the token features, the event
+    features and the segment table."""
+    w = wl.grounding_32k()
+
+    def f(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+
+    base = dict(g=f(w.g), p=f(w.p), cu=torch.from_numpy(w.cu_seg).cuda())
+    set_bytes = sum(t.numel() * t.element_size() for t in base.values())
+    nsets = max(1, math.ceil(ROTATE_BYTES / set_bytes))
+    sets = [base] + [_clone_set(base) for _ in range(nsets - 1)]
+    scores = torch.empty((w.K, w.S), dtype=torch.float32, device="cuda")
+    sal = torch.empty((w.K, w.S), dtype=torch.uint8, device="cuda")
+    ws = torch.empty(pdec.grounding_workspace_size(w.K, w.N, w.S, w.d), dtype=torch.uint8, device="cuda")
+
+    def call(i):
+        d = sets[i % nsets]
+        pdec.segment_grounding(d["g"], d["p"], d["cu"], 0.5, scores=scores, salient=sal, workspace=ws)
+
+    for i in range(args.warmup):
+        call(i)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(args.steps):
+        call(i)
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) / args.steps * 1e3
+    nbytes = w.N * w.d * 2 + w.K * w.d * 2 + (w.S + 1) * 4
+    gbps = nbytes / (us * 1e-6) / 1e9
+    _log(f"bench: grounding {us:.2f} us/call, {nbytes / 1e6:.2f} MB, sets={nsets}")
+    rec = {
+        "metric": "us per segment-similarity grounding call (32 events x 32704 tokens x 128 segments)",
+        "value": round(us, 3), "unit": "us/call", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "higher_is_better": False, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": w.name, "events": w.K, "tokens": w.N, "segments": w.S, "dim": w.d, "seed": w.seed},
+        "roofline": {"bound": "hbm", "achieved": round(gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(gbps / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "kernel": "ground_partial_kernel + ground_finish_kernel (per call)", "kernel_us": round(us, 3),
+                     "kernel_algorithmic_bytes": nbytes},
+    }
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="long_32k",
-                    help="long_32k | single_8k | ragged_16 | tiny_f32 | loop_64 | rope_append")
+                    help="long_32k | single_8k | ragged_16 | tiny_f32 | loop_64 | rope_append | grounding")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--plan-mask", choices=("full", "self"), default="full",
                     help="full: every stream sees all plan tokens (the full design); self: each stream sees only "
@@ -289,6 +340,9 @@ def main():
         return
     if args.workload == "rope_append":
         run_rope(args, torch, pdec, wl)
+        return
+    if args.workload == "grounding":
+        run_grounding(args, torch, pdec, wl)
         return
     s = wl.STEP_WORKLOADS[args.workload]()
     ragged = s.num_videos > 1

@@ -205,6 +205,42 @@ int pdec_query_plan(const pdec_dims* dims, int32_t num_videos, int32_t* path, in
  */
 int pdec_set_split_timer(void* const* start_events, void* const* stop_events, int n);
 
+/*
+ * Segment-level similarity grounding at inference (App. "More Implementation
+ * Details": grounding by feature similarity).  For the K generated global
+ * event tokens of a video and its N audio-visual prefix tokens, both already
+ * projected by the caller's two-layer MLP to width d:
+ *   score[i, s]   = sum over tokens n of segment s of <g_i, p_n>,
+ *   salient[i, s] = 1 if score[i, s] > threshold * max over s' of score[i, s'],
+ *                   else 0   (threshold 0.5 or 0.7 in the paper's experiments).
+ * Segment s is the contiguous token range [cu_seg[s], cu_seg[s+1]); an empty
+ * segment scores 0.  Scores accumulate in float32; each segment adds its
+ * per-chunk pieces in a fixed order, so repeated calls agree bit for bit.
+ */
+typedef struct pdec_ground_dims {
+    int32_t num_events;    /* K, 1..64                                              */
+    int32_t num_tokens;    /* N >= 1                                                */
+    int32_t num_segments;  /* S >= 1                                                */
+    int32_t dim;           /* d: 64, 128 or 256                                     */
+    int32_t dtype;         /* PDEC_DTYPE_BF16 (the only type with a kernel)         */
+} pdec_ground_dims;
+
+/* Workspace bytes for pdec_segment_grounding (0 for invalid dims). Host only. */
+size_t pdec_grounding_workspace_size(const pdec_ground_dims* dims);
+
+/*
+ *   g [K, d], p [N, d]           device, bf16, rows contiguous, 16-byte aligned;
+ *   cu_seg [S + 1] int32         device, non-decreasing from 0 to N (not checked:
+ *                                ranges are clamped to [0, N), so a bad table gives
+ *                                wrong scores, never a stray access);
+ *   scores [K, S] float32, salient [K, S] uint8   device, written;
+ *   workspace >= pdec_grounding_workspace_size(dims) bytes, device, contents ignored.
+ * Asynchronous on `stream` (two launches).  Returns a pdec_status.
+ */
+int pdec_segment_grounding(const pdec_ground_dims* dims, const void* g, const void* p, const int32_t* cu_seg,
+                           float threshold, float* scores, uint8_t* salient, void* workspace,
+                           size_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -27,7 +27,7 @@ PATH_AUTO, PATH_VALU, PATH_MFMA = 0, 1, 2
 
 EXPORTED = ("pdec_strerror", "pdec_workspace_size", "pdec_attn_step", "pdec_attn_step_ragged",
             "pdec_kv_append", "pdec_rope_kv_append", "pdec_set_path", "pdec_query_plan",
-            "pdec_set_split_timer")
+            "pdec_set_split_timer", "pdec_grounding_workspace_size", "pdec_segment_grounding")
 
 
 class Dims(ctypes.Structure):
@@ -39,6 +39,13 @@ class Dims(ctypes.Structure):
                 ("max_events_per_video", ctypes.c_int32), ("dtype", ctypes.c_int32),
                 ("softmax_scale", ctypes.c_float), ("prefix_tokens", ctypes.c_int64),
                 ("plan_mask", ctypes.c_int32), ("plan_tokens_per_stream", ctypes.c_int32)]
+
+
+class GroundDims(ctypes.Structure):
+    """Mirror of ``pdec_ground_dims``."""
+
+    _fields_ = [("num_events", ctypes.c_int32), ("num_tokens", ctypes.c_int32),
+                ("num_segments", ctypes.c_int32), ("dim", ctypes.c_int32), ("dtype", ctypes.c_int32)]
 
 
 class PdecError(RuntimeError):
@@ -76,6 +83,11 @@ def lib():
         L.pdec_kv_append.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp]
         L.pdec_rope_kv_append.restype = ctypes.c_int
         L.pdec_rope_kv_append.argtypes = [dp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_float, vp]
+        gp = ctypes.POINTER(GroundDims)
+        L.pdec_grounding_workspace_size.restype = ctypes.c_size_t
+        L.pdec_grounding_workspace_size.argtypes = [gp]
+        L.pdec_segment_grounding.restype = ctypes.c_int
+        L.pdec_segment_grounding.argtypes = [gp, vp, vp, vp, ctypes.c_float, vp, vp, vp, sz, vp]
         L.pdec_set_path.restype = ctypes.c_int
         L.pdec_set_path.argtypes = [ctypes.c_int]
         L.pdec_query_plan.restype = ctypes.c_int
@@ -267,6 +279,37 @@ def rope_kv_append(q, k_new, v_new, k_event, v_event, event_lens, pos_base, live
             _dev(pos_base, "pos_base", torch.int32, 1)]
     _check("pdec_rope_kv_append", lib().pdec_rope_kv_append(ctypes.byref(dims), V, *args, float(theta),
                                                             _stream(stream, q.device)))
+
+
+def grounding_workspace_size(K, N, S, d, dtype_code=1) -> int:
+    return int(lib().pdec_grounding_workspace_size(ctypes.byref(GroundDims(K, N, S, d, dtype_code))))
+
+
+def segment_grounding(g, p, cu_seg, threshold, *, scores=None, salient=None, workspace=None, stream=None):
+    """Segment scores and saliency of every event (``pdec_segment_grounding``).
+
+    g [K,d], p [N,d] bf16; cu_seg int32 [S+1].  Returns (scores float32 [K,S],
+    salient uint8 [K,S]).
+    """
+    K, d = g.shape
+    N = p.shape[0]
+    S = cu_seg.shape[0] - 1
+    if p.shape != (N, d):
+        raise ValueError("g and p must have the same feature width")
+    dims = GroundDims(K, N, S, d, _dtype_code(g))
+    if scores is None:
+        scores = torch.empty((K, S), dtype=torch.float32, device=g.device)
+    if salient is None:
+        salient = torch.empty((K, S), dtype=torch.uint8, device=g.device)
+    ws_bytes = int(lib().pdec_grounding_workspace_size(ctypes.byref(dims)))
+    if workspace is None:
+        workspace = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device=g.device)
+    args = [_dev(g, "g", None, 2), _dev(p, "p", g.dtype, 2), _dev(cu_seg, "cu_seg", torch.int32, 1),
+            ctypes.c_float(float(threshold)), _dev(scores, "scores", torch.float32, 2),
+            _dev(salient, "salient", torch.uint8, 2), ctypes.c_void_p(workspace.data_ptr()),
+            ctypes.c_size_t(workspace.numel() * workspace.element_size()), _stream(stream, g.device)]
+    _check("pdec_segment_grounding", lib().pdec_segment_grounding(ctypes.byref(dims), *args))
+    return scores, salient
 
 
 class SplitTimer:

@@ -247,3 +247,66 @@ STEP_WORKLOADS = {
     "long_32k": long_32k,
     "ragged_16": ragged_16,
 }
+
+
+@dataclass
+class GroundingInputs:
+    """Projected event tokens g [K, d] and audio-visual tokens p [N, d] (bf16
+    bit patterns) with contiguous time segments cu_seg [S + 1]."""
+    name: str
+    g: np.ndarray
+    p: np.ndarray
+    cu_seg: np.ndarray
+    seed: int
+
+    @property
+    def K(self) -> int:
+        return self.g.shape[0]
+
+    @property
+    def N(self) -> int:
+        return self.p.shape[0]
+
+    @property
+    def S(self) -> int:
+        return self.cu_seg.shape[0] - 1
+
+    @property
+    def d(self) -> int:
+        return self.g.shape[1]
+
+
+def make_grounding(*, name="grounding", K=13, N=1000, S=8, d=256, sigma=0.5, seed=0, sizes=None,
+                   planted=True) -> GroundingInputs:
+    """Segment sizes are `sizes` when given (summing to N), else a random
+    split of N into S parts (some may be empty).  With `planted`, event i
+    gets a direction shared with the tokens of segment (3i mod S), so every
+    event has a clear best segment, as trained grounding features would."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    if sizes is None:
+        cuts = np.sort(rng.integers(0, N + 1, size=S - 1))
+        cu = np.concatenate([[0], cuts, [N]]).astype(np.int32)
+    else:
+        cu = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+        assert cu[-1] == N and cu.shape[0] == S + 1
+    g = (rng.standard_normal((K, d)) * sigma).astype(np.float32)
+    p = (rng.standard_normal((N, d)) * sigma).astype(np.float32)
+    if planted:
+        for i in range(K):
+            s = (3 * i) % S
+            u = rng.standard_normal(d).astype(np.float32)
+            u /= np.linalg.norm(u)
+            g[i] += 2.0 * u
+            p[cu[s]:cu[s + 1]] += 0.25 * u
+    return GroundingInputs(name, bf16_bits(g), bf16_bits(p), cu, seed)
+
+
+def grounding_32k(seed: int = 5) -> GroundingInputs:
+    """The 32k prefix's audio-visual part (32704 tokens) cut into 128 time
+    segments (256 frames at 0.5 FPS in 2 s segments), segment sizes around
+    255 tokens; 32 event tokens (the 32k step's streams); features of width
+    256 after the projection."""
+    rng = np.random.Generator(np.random.PCG64(seed + 1000))
+    sizes = rng.integers(200, 311, size=128)
+    sizes[-1] += 32704 - int(sizes.sum())
+    return make_grounding(name="grounding_N32704_S128_K32", K=32, N=32704, S=128, d=256, seed=seed, sizes=sizes)
