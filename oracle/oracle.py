@@ -64,6 +64,10 @@ def _load():
             fn.restype = ctypes.c_int
             fn.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
                            ctypes.c_void_p]
+            fn = getattr(lib, f"oracle_attn_prefill_{sfx}")
+            fn.restype = ctypes.c_int
+            fn.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p] + [ctypes.c_int] * 5 + \
+                [ctypes.c_double, ctypes.c_int] + [ctypes.c_void_p] * 8 + [ctypes.c_int]
             fn = getattr(lib, f"oracle_rope_append_{sfx}")
             fn.restype = ctypes.c_int
             fn.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p] + [ctypes.c_int] * 4 + \
@@ -211,3 +215,32 @@ def rope_append(q, k_new, event_lens, live, cu_events=None, pos_base=None, cap=N
     if rc != 0:
         raise ValueError("oracle_rope_append rejected its arguments")
     return q_rot, k_rot, new_lens
+
+
+def attn_prefill(q, k_prefix, v_prefix, k_event, v_event, event_lens, cu_prefix, cu_events, scale: float = 0.0,
+                 threads: int = 0, precision: str = "f64"):
+    """Event-factorized attention over whole branches (``oracle_attn_prefill``).
+
+    q [SE, N, H_q, D]; other tensors as for ``attn_step``.  Query j of stream
+    e sees the prefix and its own rows 0 .. min(j, n_e - 1).  Returns
+    (out [SE, N, H_q, D], lse [SE, N, H_q]).
+    """
+    lib = _load()
+    real = np.float64 if precision == "f64" else np.float32
+    fn = getattr(lib, f"oracle_attn_prefill_{precision}")
+    q, k_prefix, v_prefix, k_event, v_event = (_c(x) for x in (q, k_prefix, v_prefix, k_event, v_event))
+    dt = _dtype_code(q)
+    SE, N, H_q, D = q.shape
+    H_kv = k_prefix.shape[1]
+    cap = k_event.shape[1]
+    cu_prefix = _c(cu_prefix, np.int32)
+    cu_events = _c(cu_events, np.int32)
+    V = cu_prefix.shape[0] - 1
+    event_lens = _c(event_lens, np.int32)
+    out = np.full((SE, N, H_q, D), np.nan, dtype=real)
+    lse = np.full((SE, N, H_q), np.nan, dtype=real)
+    rc = fn(V, _ptr(cu_prefix), _ptr(cu_events), N, H_q, H_kv, D, cap, float(scale), dt, _ptr(q), _ptr(k_prefix),
+            _ptr(v_prefix), _ptr(k_event), _ptr(v_event), _ptr(event_lens), _ptr(out), _ptr(lse), int(threads))
+    if rc != 0:
+        raise ValueError("oracle_attn_prefill rejected its arguments")
+    return out, lse

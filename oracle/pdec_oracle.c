@@ -35,6 +35,10 @@
  *     tokens are: the plan segment is taken as the last E*T prefix tokens,
  *     stream f's tokens being the f-th run of T of them (T tokens per
  *     stream, in stream order).
+ *   - whole branches at once (oracle_attn_prefill, the training / prefill
+ *     form): query j of a branch is the decode step of that branch at its
+ *     token j, i.e. it sees its own rows 0 .. j (§3.4 pads branches to the
+ *     longest with EOS when training; a branch with fewer rows stops there).
  *   - the rotary embedding at the shared step position (oracle_rope_append)
  *     is taken in the rotate-half form with frequencies theta^(-2i/D); a
  *     stream writing cache row t of video v stands at pos_base[v] + t.
@@ -285,6 +289,52 @@ int ORACLE_FN(oracle_decode_loop)(int steps, int E, int H_q, int H_kv, int D, in
     free(kc);
     free(vc);
     free(n);
+    return rc;
+}
+
+/*
+ * Event-factorized attention over whole branches at once: the prefill /
+ * training form of the §3.4 mask (the full-sequence picture of Fig. 3).
+ * Stream e holds n_e rows of its own branch (§3.4 trains with the branches
+ * padded by EOS to the longest, N); its query j, 0 <= j < N, sees every
+ * prefix token and its own rows 0 .. min(j, n_e - 1), never another branch.
+ * Query j of stream e is therefore the decode step of stream e holding
+ * min(j + 1, n_e) rows, and the oracle evaluates exactly that, one step per
+ * j.  A stream with n_e == 0 has no branch: its rows are 0 and -inf.
+ *   q [SE, N, H_q, D];  out [SE, N, H_q, D], lse [SE, N, H_q]  (real);
+ *   other arguments as for oracle_attn_step (no plan mask).
+ */
+int ORACLE_FN(oracle_attn_prefill)(int num_videos, const int32_t* cu_prefix, const int32_t* cu_events, int N,
+                                   int H_q, int H_kv, int D, int cap, double scale, int dtype, const void* q,
+                                   const void* k_prefix, const void* v_prefix, const void* k_event,
+                                   const void* v_event, const int32_t* n, real* out, real* lse, int num_threads)
+{
+    if (num_videos < 1 || N < 1) return -1;
+    const int SE = cu_events[num_videos];
+    const size_t esz = dtype == 0 ? 4 : 2;
+    const size_t qrow = (size_t)H_q * D * esz;  /* one query token, all heads */
+    unsigned char* qj = (unsigned char*)malloc((size_t)SE * qrow + 1);
+    int32_t* nj = (int32_t*)malloc((size_t)SE * sizeof(int32_t) + 4);
+    real* oj = (real*)malloc((size_t)SE * H_q * D * sizeof(real) + 8);
+    real* lj = (real*)malloc((size_t)SE * H_q * sizeof(real) + 8);
+    int rc = (qj && nj && oj && lj) ? 0 : -1;
+    for (int j = 0; j < N && rc == 0; ++j) {
+        for (int e = 0; e < SE; ++e) {
+            memcpy(qj + (size_t)e * qrow, (const unsigned char*)q + ((size_t)e * N + j) * qrow, qrow);
+            nj[e] = n[e] <= 0 ? 0 : (j + 1 < n[e] ? j + 1 : n[e]);
+        }
+        rc = ORACLE_FN(oracle_attn_step)(num_videos, cu_prefix, cu_events, H_q, H_kv, D, cap, scale, dtype, 0, 0,
+                                         qj, k_prefix, v_prefix, k_event, v_event, nj, NULL, oj, lj, NULL,
+                                         num_threads);
+        for (int e = 0; e < SE && rc == 0; ++e) {
+            memcpy(out + ((size_t)e * N + j) * H_q * D, oj + (size_t)e * H_q * D, (size_t)H_q * D * sizeof(real));
+            memcpy(lse + ((size_t)e * N + j) * H_q, lj + (size_t)e * H_q, (size_t)H_q * sizeof(real));
+        }
+    }
+    free(qj);
+    free(nj);
+    free(oj);
+    free(lj);
     return rc;
 }
 

@@ -36,6 +36,9 @@ MUTANTS = {
     "rope_pair_partner": ("load_elem(x, base + i + half, dtype);", "load_elem(x, base + (i ^ 1), dtype);"),
     "rope_position_off_by_one": ("(real)pos_base[v] + (real)t;", "(real)pos_base[v] + (real)t + 1;"),
     "rope_ended_keeps_count": ("new_lens[e] = 0;", "new_lens[e] = t;"),
+    "prefill_row_off_by_one": ("(j + 1 < n[e] ? j + 1 : n[e])", "(j < n[e] ? j : n[e])"),
+    "prefill_not_causal": ("(j + 1 < n[e] ? j + 1 : n[e])", "n[e]"),
+    "prefill_wrong_token": ("((size_t)e * N + j) * qrow, qrow);", "((size_t)e * N + 0) * qrow, qrow);"),
 }
 
 

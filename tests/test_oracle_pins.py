@@ -627,3 +627,62 @@ def test_rope_bf16_inputs_are_widened_exactly():
     a = oracle.rope_append(qb, kb, lens, [1] * 5, pos_base=[77])
     b = oracle.rope_append(qf, kf, lens, [1] * 5, pos_base=[77])
     assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+
+
+# ---- whole branches at once (the prefill / training form of the mask) ----
+
+def _prefill_case(seed, E=3, N=5, L=7, H_q=4, H_kv=2, D=8, lens=(5, 3, 0)):
+    rng = np.random.default_rng(seed)
+    q = rng.standard_normal((E, N, H_q, D)).astype(np.float32)
+    kp = rng.standard_normal((L, H_kv, D)).astype(np.float32)
+    vp = rng.standard_normal((L, H_kv, D)).astype(np.float32)
+    ke = rng.standard_normal((E, N, H_kv, D)).astype(np.float32)
+    ve = rng.standard_normal((E, N, H_kv, D)).astype(np.float32)
+    return q, kp, vp, ke, ve, np.array(lens, np.int32)
+
+
+def test_prefill_zero_keys_average_exactly_the_visible_rows():
+    """With every key 0 all scores tie, so query j of branch e returns the
+    plain mean of the value rows it may see: the prefix and its own rows
+    0 .. min(j, n_e - 1) (§3.4, Fig. 3), written out here with numpy means."""
+    q, kp, vp, ke, ve, n = _prefill_case(1)
+    kp[:] = 0
+    ke[:] = 0
+    out, lse = oracle.attn_prefill(q, kp, vp, ke, ve, n, [0, kp.shape[0]], [0, 3])
+    G = q.shape[2] // kp.shape[1]
+    for e in range(3):
+        for j in range(q.shape[1]):
+            if n[e] == 0:
+                assert np.all(out[e, j] == 0) and np.all(np.isneginf(lse[e, j]))
+                continue
+            vis = min(j + 1, n[e])
+            for h in range(q.shape[2]):
+                g = h // G
+                rows = np.concatenate([vp[:, g], ve[e, :vis, g]]).astype(np.float64)
+                np.testing.assert_allclose(out[e, j, h], rows.mean(axis=0), atol=1e-12)
+                assert abs(lse[e, j, h] - math.log(rows.shape[0])) < 1e-12
+
+
+def test_prefill_is_causal_inside_a_branch_and_blind_to_others():
+    """Changing branch rows after j leaves query j of that branch unchanged;
+    changing one branch leaves every other branch unchanged (bitwise)."""
+    q, kp, vp, ke, ve, n = _prefill_case(2, lens=(5, 5, 4))
+    out, _ = oracle.attn_prefill(q, kp, vp, ke, ve, n, [0, kp.shape[0]], [0, 3])
+    ke2, ve2 = ke.copy(), ve.copy()
+    ke2[0, 3:] += 5.0
+    ve2[0, 3:] -= 7.0
+    out2, _ = oracle.attn_prefill(q, kp, vp, ke2, ve2, n, [0, kp.shape[0]], [0, 3])
+    assert np.array_equal(out2[0, :3], out[0, :3])
+    assert not np.allclose(out2[0, 3:], out[0, 3:])
+    assert np.array_equal(out2[1:], out[1:])
+
+
+def test_prefill_query_equals_the_decode_step_at_that_token():
+    """Query j of branch e is the decode step of branch e holding j + 1 rows
+    (row a4's step over the same caches)."""
+    q, kp, vp, ke, ve, n = _prefill_case(3, lens=(5, 2, 4))
+    out, lse = oracle.attn_prefill(q, kp, vp, ke, ve, n, [0, kp.shape[0]], [0, 3])
+    j = 3
+    o, l = oracle.attn_step(np.ascontiguousarray(q[:, j]), kp, vp, ke, ve, np.minimum(j + 1, n), [0, kp.shape[0]],
+                            [0, 3])
+    assert np.array_equal(out[:, j], o) and np.array_equal(lse[:, j], l)
