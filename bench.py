@@ -298,13 +298,66 @@ def run_grounding(args, torch, pdec, wl):
     print(json.dumps(rec), flush=True)
 
 
+def run_prefill(args, torch, pdec, wl):
+    """Whole branches at once (the prefill / training form of the mask):
+    13 branches (the paper's mean subchain count) of 48 tokens each over a
+    32768-token prefix, H_q 28, H_kv 4, D 128, bf16.  Each of the 624 query
+    tokens x 28 heads sees the whole prefix and its own branch up to itself.
+    This is a dense contraction, so its roofline is the matrix cores':
+    algorithmic flops = 4 * D * sum over query rows of their visible keys.
+    µs per call from HIP events around K back-to-back calls."""
+    E, N, L, H_q, H_kv, D = 13, 48, 32768, 28, 4, 128
+    rng = np.random.default_rng(6)
+
+    def f(*shape):
+        a = wl.bf16_bits((0.5 * rng.standard_normal(shape)).astype(np.float32))
+        return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
+
+    q, kp, vp, ke, ve = f(E, N, H_q, D), f(L, H_kv, D), f(L, H_kv, D), f(E, N, H_kv, D), f(E, N, H_kv, D)
+    lens = torch.full((E,), N, dtype=torch.int32, device="cuda")
+    plen = torch.tensor([L], dtype=torch.int32, device="cuda")
+    out = torch.empty_like(q)
+    lse = torch.empty((E, N, H_q), dtype=torch.float32, device="cuda")
+    dims = pdec.make_dims(E, H_q, H_kv, D, N, L, pdec.PDEC_DTYPE_BF16, queries_per_stream=N)
+    ws = torch.empty(pdec.workspace_size(dims), dtype=torch.uint8, device="cuda")
+
+    def call():
+        pdec.attn_prefill(q, kp, vp, ke, ve, lens, plen, out=out, lse=lse, workspace=ws)
+
+    for _ in range(args.warmup):
+        call()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        call()
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) / args.steps * 1e3
+    keys = E * H_q * sum(L + j + 1 for j in range(N))  # visible keys summed over query rows
+    flops = 4 * D * keys
+    tflops = flops / (us * 1e-6) / 1e12
+    _log(f"bench: prefill {us:.1f} us/call, {flops / 1e9:.1f} GFLOP, {tflops:.1f} TFLOP/s")
+    rec = {
+        "metric": "us per whole-branch attention call (13 branches x 48 tokens over a 32768-token prefix)",
+        "value": round(us, 2), "unit": "us/call", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "higher_is_better": False, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "prefill_L32768_E13_N48", "prefix_len": L, "branches": E, "tokens_per_branch": N,
+                   "H_q": H_q, "H_kv": H_kv, "head_dim": D},
+        "roofline": {"bound": "mfma", "achieved": round(tflops, 1), "peak": 2500.0, "unit": "TFLOP/s",
+                     "frac": round(tflops / 2500.0, 4), "traffic": None, "kernel": "split pass + finish (per call)",
+                     "kernel_us": round(us, 2), "kernel_algorithmic_flops": flops},
+    }
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="long_32k",
-                    help="long_32k | single_8k | ragged_16 | tiny_f32 | loop_64 | rope_append | grounding")
+                    help="long_32k | single_8k | ragged_16 | tiny_f32 | loop_64 | rope_append | grounding | prefill")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--plan-mask", choices=("full", "self"), default="full",
                     help="full: every stream sees all plan tokens (the full design); self: each stream sees only "
@@ -343,6 +396,9 @@ def main():
         return
     if args.workload == "grounding":
         run_grounding(args, torch, pdec, wl)
+        return
+    if args.workload == "prefill":
+        run_prefill(args, torch, pdec, wl)
         return
     s = wl.STEP_WORKLOADS[args.workload]()
     ragged = s.num_videos > 1

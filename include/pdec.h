@@ -84,6 +84,13 @@ typedef struct pdec_dims {
                                   /* is meant for E*T <= L; beyond that the runs keep their     */
                                   /* places counted from L - E*T and the parts before prefix    */
                                   /* key 0 do not exist.  0 means no plan segment.  Must be >= 0 */
+    int32_t queries_per_stream;   /* Q; 0 or 1: one query per stream, the decode step.  Q > 1:   */
+                                  /* whole branches at once (the prefill / training form of     */
+                                  /* §3.4's mask, Fig. 3): q and out are [num_events, Q, H_q, D], */
+                                  /* lse [num_events, Q, H_q], and query j of stream e sees the   */
+                                  /* prefix and its own rows 0 .. min(j, n_e - 1), never another  */
+                                  /* stream's; n_e == 0 gives rows of 0 / -inf.  Q > 1 needs      */
+                                  /* bfloat16 and plan_mask == 0 (else PDEC_ERR_UNSUPPORTED).    */
 } pdec_dims;
 
 /* Human-readable text of a pdec_status code.  Never NULL. */
@@ -110,7 +117,9 @@ size_t pdec_workspace_size(const pdec_dims* dims, int32_t num_videos);
  *   out         [E, H_q, D]            written for every row
  *   lse         [E, H_q] float32, or NULL to skip it
  *   workspace   device, >= pdec_workspace_size(dims, 1) bytes, contents ignored
- * E = dims->num_events.  Returns a pdec_status.
+ * E = dims->num_events.  With dims->queries_per_stream = Q > 1 the call
+ * evaluates whole branches: q and out are [E, Q, H_q, D], lse [E, Q, H_q]
+ * (see pdec_dims).  Returns a pdec_status.
  */
 int pdec_attn_step(const pdec_dims* dims, const void* q, const void* k_prefix, const void* v_prefix,
                    const void* k_event, const void* v_event, const int32_t* event_lens,

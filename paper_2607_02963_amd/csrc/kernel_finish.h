@@ -54,7 +54,7 @@ __global__ __launch_bounds__(256) void finish_kernel(StepArgs a)
     const int wave = tid >> 6;
     const int lane = tid & 63;
     const long qr = blockIdx.x;  // (stream, head) row
-    const int e = (int)(qr / a.H_q);
+    const int e = (int)(qr / ((long)a.H_q * a.qps));
     T* __restrict__ out = static_cast<T*>(a.out) + qr * D;
 
     if (a.event_lens[e] <= 0) {  // ended stream: uniform over the work-group

@@ -114,7 +114,7 @@ __device__ inline int k_off(int key, int ch) { return key * (2 * D) + 16 * (ch ^
 template <int D>
 __device__ inline int v_off(int key, int ch) { return key * (2 * D) + 16 * (ch ^ ((2 * key) & 6)); }
 
-template <int D, int NT, int WR, int WK, bool PLAN>
+template <int D, int NT, int WR, int WK, bool PLAN, bool MQ>
 __global__ __launch_bounds__(512) void split_mfma_kernel(StepArgs a)
 {
     using C = MfmaCfg<D, NT, WR, WK>;
@@ -128,7 +128,7 @@ __global__ __launch_bounds__(512) void split_mfma_kernel(StepArgs a)
     if (item < 0) return;
     const ItemId id = item_id(a, item);
     const VideoInfo vi = video_info(a, id.v);
-    const int R = vi.E * a.G;
+    const int R = vi.E * a.G * a.qps;
     const int row0 = id.rg * C::RT;
     if (row0 >= R) return;
     const int nrows = min(C::RT, R - row0);
@@ -170,6 +170,7 @@ __global__ __launch_bounds__(512) void split_mfma_kernel(StepArgs a)
     const int wrow0 = row0 + 16 * rw * NT;                // first video row of this wave
     const bool row_wave_active = 16 * rw * NT < nrows;
     int lane_stream[NT];
+    int lane_tok[NT];  // query token of the row within its stream (whole branches; 0 otherwise)
     bf16x8_t qf[NT][C::KSTEPS];  // Q^T operands: q[row][32t + 8lg .. +7]
     {
         const uint16_t* __restrict__ q = static_cast<const uint16_t*>(a.q);
@@ -177,7 +178,8 @@ __global__ __launch_bounds__(512) void split_mfma_kernel(StepArgs a)
         for (int nt = 0; nt < NT; ++nt) {
             const int r = 16 * (rw * NT + nt) + l16;
             const bool ok = r < nrows;
-            lane_stream[nt] = ok ? (row0 + r) / a.G : -2;
+            lane_stream[nt] = ok ? (row0 + r) / (a.G * a.qps) : -2;
+            lane_tok[nt] = ok ? ((row0 + r) / a.G) % a.qps : 0;
             const long base = ok ? (long)row_qrow(a, vi, id.g, row0 + r) * D : 0;
 #pragma unroll
             for (int t = 0; t < C::KSTEPS; ++t) {
@@ -286,8 +288,12 @@ __global__ __launch_bounds__(512) void split_mfma_kernel(StepArgs a)
                     for (int i = 0; i < 4; ++i) {
                         const bool kout = kb + 16 * kt + 4 * lg + i >= ui.nk;
 #pragma unroll
-                        for (int nt = 0; nt < NT; ++nt)
-                            if (kout || (ui.stream >= 0 && lane_stream[nt] != ui.stream)) s[kt][nt][i] = kNegInf;
+                        for (int nt = 0; nt < NT; ++nt) {
+                            bool hide = kout || (ui.stream >= 0 && lane_stream[nt] != ui.stream);
+                            // whole branches: query j sees its own rows 0 .. j only
+                            if constexpr (MQ) hide = hide || (ui.stream >= 0 && ui.k0 + kb + 16 * kt + 4 * lg + i > lane_tok[nt]);
+                            if (hide) s[kt][nt][i] = kNegInf;
+                        }
                     }
             }
         }
@@ -355,7 +361,7 @@ __global__ __launch_bounds__(512) void split_mfma_kernel(StepArgs a)
         // an own unit of stream f only concerns the rows of f
         bool wave_has_rows = row_wave_active;
         if (ui.stream >= 0) {
-            const int f0 = ui.stream * a.G, f1 = f0 + a.G;  // video rows of stream f
+            const int f0 = ui.stream * a.G * a.qps, f1 = f0 + a.G * a.qps;  // video rows of stream f
             wave_has_rows = wave_has_rows && f0 < wrow0 + 16 * NT && f1 > wrow0;
         }
         const unsigned char* kbuf = lds + (st % C::NSTAGE) * C::STAGE;

@@ -71,8 +71,12 @@ int validate_dims(const pdec_dims* d, int num_videos)
     if (num_videos < 1 || d->num_events < 1 || d->num_q_heads < 1 || d->num_kv_heads < 1 ||
         d->num_q_heads % d->num_kv_heads != 0 || d->event_cap < 1 || d->max_prefix_len < 0 ||
         d->max_events_per_video < 0 || d->max_events_per_video > d->num_events || d->prefix_tokens < 0 ||
-        d->plan_mask < 0 || d->plan_mask > 1 || d->plan_tokens_per_stream < 0)
+        d->plan_mask < 0 || d->plan_mask > 1 || d->plan_tokens_per_stream < 0 || d->queries_per_stream < 0)
         return PDEC_ERR_INVALID_ARG;
+    // whole branches run on the matrix-core kernel only, without the plan mask
+    if (d->queries_per_stream > 1 &&
+        (d->dtype != PDEC_DTYPE_BF16 || (d->plan_mask && d->plan_tokens_per_stream > 0)))
+        return PDEC_ERR_UNSUPPORTED;
     if (d->dtype != PDEC_DTYPE_F32 && d->dtype != PDEC_DTYPE_BF16) return PDEC_ERR_UNSUPPORTED;
     if (d->head_dim != 64 && d->head_dim != 128) return PDEC_ERR_UNSUPPORTED;
     if (!(d->softmax_scale <= 0.f) && !std::isfinite(d->softmax_scale)) return PDEC_ERR_INVALID_ARG;
@@ -84,7 +88,8 @@ int validate_dims(const pdec_dims* d, int num_videos)
     if (d->plan_mask && (long)d->plan_tokens_per_stream * events_per_video(d) > (1L << 30))
         return PDEC_ERR_UNSUPPORTED;
     // index arithmetic inside the kernels is 32-bit for row counts
-    if ((long)d->num_events * d->num_q_heads > (1L << 30)) return PDEC_ERR_UNSUPPORTED;
+    if ((long)d->num_events * d->num_q_heads * std::max(d->queries_per_stream, 1) > (1L << 30))
+        return PDEC_ERR_UNSUPPORTED;
     return PDEC_OK;
 }
 
@@ -93,11 +98,13 @@ Plan make_plan(const pdec_dims* d, int num_videos)
     Plan p{};
     const int G = d->num_q_heads / d->num_kv_heads;
     const int ev = events_per_video(d);
-    const long rows_max = (long)ev * G;  // query rows per (video, kv head)
+    const int qps = std::max(d->queries_per_stream, 1);
+    const long rows_max = (long)ev * G * qps;  // query rows per (video, kv head)
     int path = (d->dtype == PDEC_DTYPE_BF16 && rows_max >= 16) ? kPathMfma : kPathValu;
     const int ov = g_path_override.load();
     if (ov == kPathValu) path = kPathValu;
     if (ov == kPathMfma && d->dtype == PDEC_DTYPE_BF16) path = kPathMfma;
+    if (qps > 1) path = kPathMfma;  // the vector kernels take one query per stream
     p.path = path;
     if (path == kPathMfma) {
         // 8 waves: up to 4 tiles -> 1 tile per row wave, 2 key groups (64 rows);
@@ -130,7 +137,7 @@ Plan make_plan(const pdec_dims* d, int num_videos)
     p.unit_per_chunk = (int)std::min<long>(upc, 1L << 24);
     p.max_chunks = (int)std::max<long>(1, ceil_div(units_max, p.unit_per_chunk));
     p.n_items = (long)num_videos * d->num_kv_heads * p.max_chunks * p.rg_max;
-    const size_t rows = (size_t)d->num_events * d->num_q_heads;
+    const size_t rows = (size_t)d->num_events * d->num_q_heads * std::max(d->queries_per_stream, 1);
     const size_t elem = d->dtype == PDEC_DTYPE_BF16 ? 2 : 4;
     p.part_o_bytes = (size_t)p.max_chunks * rows * d->head_dim * elem;  // a multiple of 128 bytes
     p.part_ml_bytes = (size_t)p.max_chunks * rows * 2 * sizeof(float);
@@ -198,7 +205,7 @@ int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_pr
     a.prefix_len = cu_prefix ? nullptr : prefix_len;
     a.out = out;
     a.lse = lse;
-    const size_t rows = (size_t)d->num_events * d->num_q_heads;
+    const size_t rows = (size_t)d->num_events * d->num_q_heads * std::max(d->queries_per_stream, 1);
     a.part_o = workspace;
     a.part_ml = reinterpret_cast<float*>(static_cast<char*>(workspace) + p.part_o_bytes);
     a.video_chunks = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + p.part_o_bytes + p.part_ml_bytes);
@@ -219,6 +226,7 @@ int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_pr
     const float scale = d->softmax_scale > 0.f ? d->softmax_scale : 1.f / std::sqrt((float)d->head_dim);
     a.qscale = scale * 1.4426950408889634f;
     a.plan_T = d->plan_mask ? d->plan_tokens_per_stream : 0;
+    a.qps = std::max(d->queries_per_stream, 1);
 
     hipStream_t s = static_cast<hipStream_t>(stream);
     const int grid = 8 * a.items_per_xcd;

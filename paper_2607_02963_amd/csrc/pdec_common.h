@@ -60,6 +60,7 @@ struct StepArgs {
     int items_per_xcd;          // ceil(n_items / 8)
     float qscale;               // softmax scale * log2(e)
     int plan_T;                 // plan tokens per stream when the self-only plan mask is on, else 0
+    int qps;                    // queries per stream: 1 for a decode step, N for whole branches
 };
 
 // Launch of the matrix-core split pass (its own translation unit).
@@ -209,10 +210,14 @@ __device__ inline bool plan_key_hidden(const StepArgs& a, const VideoInfo& vi, i
     return (j >= vi.plan0) & ((j < lo) | (j >= lo + a.plan_T));
 }
 
-// Global (stream, head) row of item row r (r counted from 0 within the video).
+// Global query row of item row r (r counted from 0 within the video).  A
+// video's rows of one kv head are stream-major, then query token, then the
+// head within the group: r = (f * qps + j) * G + h.
 __device__ inline int row_qrow(const StepArgs& a, const VideoInfo& vi, int g, int r)
 {
-    return (vi.e0 + r / a.G) * a.H_q + g * a.G + r % a.G;
+    const int per_stream = a.G * a.qps;
+    const int f = r / per_stream, rem = r - f * per_stream, j = rem / a.G, h = rem - j * a.G;
+    return ((vi.e0 + f) * a.qps + j) * a.H_q + g * a.G + h;
 }
 
 // Element conversions.  bf16 travels as its 16-bit pattern.

@@ -13,29 +13,32 @@ namespace pdec {
 
 namespace {
 
-template <int D, bool PLAN>
+template <int D, bool PLAN, bool MQ>
 void launch_shape(const StepArgs& a, int shape, int grid, hipStream_t s)
 {
     switch (shape) {
-    case 1: hipLaunchKernelGGL((split_mfma_kernel<D, 1, 4, 2, PLAN>), dim3(grid), dim3(512), 0, s, a); break;
-    case 2: hipLaunchKernelGGL((split_mfma_kernel<D, 2, 4, 2, PLAN>), dim3(grid), dim3(512), 0, s, a); break;
-    default: hipLaunchKernelGGL((split_mfma_kernel<D, 2, 8, 1, PLAN>), dim3(grid), dim3(512), 0, s, a); break;
+    case 1: hipLaunchKernelGGL((split_mfma_kernel<D, 1, 4, 2, PLAN, MQ>), dim3(grid), dim3(512), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((split_mfma_kernel<D, 2, 4, 2, PLAN, MQ>), dim3(grid), dim3(512), 0, s, a); break;
+    default: hipLaunchKernelGGL((split_mfma_kernel<D, 2, 8, 1, PLAN, MQ>), dim3(grid), dim3(512), 0, s, a); break;
     }
 }
 
 }  // namespace
 
-// The self-only plan mask has kernels of its own, so that the full design's
-// inner loop carries none of its tests.
+// The self-only plan mask and whole branches (several queries per stream)
+// have kernels of their own, so that the decode step's inner loop carries
+// none of their tests.  The two are not combined (the host refuses it).
 void launch_split_mfma(const StepArgs& a, int shape, int grid, hipStream_t stream)
 {
-    const bool plan = a.plan_T > 0;
+    const bool plan = a.plan_T > 0, mq = a.qps > 1;
     if (a.D == 128) {
-        if (plan) launch_shape<128, true>(a, shape, grid, stream);
-        else launch_shape<128, false>(a, shape, grid, stream);
+        if (mq) launch_shape<128, false, true>(a, shape, grid, stream);
+        else if (plan) launch_shape<128, true, false>(a, shape, grid, stream);
+        else launch_shape<128, false, false>(a, shape, grid, stream);
     } else {
-        if (plan) launch_shape<64, true>(a, shape, grid, stream);
-        else launch_shape<64, false>(a, shape, grid, stream);
+        if (mq) launch_shape<64, false, true>(a, shape, grid, stream);
+        else if (plan) launch_shape<64, true, false>(a, shape, grid, stream);
+        else launch_shape<64, false, false>(a, shape, grid, stream);
     }
 }
 

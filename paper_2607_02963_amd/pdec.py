@@ -38,7 +38,8 @@ class Dims(ctypes.Structure):
                 ("event_cap", ctypes.c_int32), ("max_prefix_len", ctypes.c_int32),
                 ("max_events_per_video", ctypes.c_int32), ("dtype", ctypes.c_int32),
                 ("softmax_scale", ctypes.c_float), ("prefix_tokens", ctypes.c_int64),
-                ("plan_mask", ctypes.c_int32), ("plan_tokens_per_stream", ctypes.c_int32)]
+                ("plan_mask", ctypes.c_int32), ("plan_tokens_per_stream", ctypes.c_int32),
+                ("queries_per_stream", ctypes.c_int32)]
 
 
 class GroundDims(ctypes.Structure):
@@ -135,10 +136,11 @@ def _stream(stream, device) -> ctypes.c_void_p:
 
 
 def make_dims(num_events, H_q, H_kv, D, cap, max_prefix_len, dtype_code, scale=0.0,
-              max_events_per_video=0, prefix_tokens=0, plan_mask=0, plan_per_stream=0) -> Dims:
+              max_events_per_video=0, prefix_tokens=0, plan_mask=0, plan_per_stream=0,
+              queries_per_stream=0) -> Dims:
     return Dims(int(num_events), int(H_q), int(H_kv), int(D), int(cap), int(max_prefix_len),
                 int(max_events_per_video), int(dtype_code), float(scale), int(prefix_tokens), int(plan_mask),
-                int(plan_per_stream))
+                int(plan_per_stream), int(queries_per_stream))
 
 
 def workspace_size(dims: Dims, num_videos: int = 1) -> int:
@@ -203,6 +205,41 @@ def attn_step(q, k_prefix, v_prefix, k_event, v_event, event_lens, prefix_lens, 
         raise ValueError("head dims disagree")
     if event_lens.shape[0] != E or out.shape != q.shape:
         raise ValueError("event_lens / out shape")
+    _check("pdec_attn_step", lib().pdec_attn_step(ctypes.byref(dims), *args))
+    return out, lse
+
+
+def attn_prefill(q, k_prefix, v_prefix, k_event, v_event, event_lens, prefix_lens, *, out=None, lse=None,
+                 workspace=None, max_prefix_len=None, scale=0.0, stream=None):
+    """Whole branches of one video at once (``queries_per_stream`` N in
+    pdec_dims); returns (out [E,N,H_q,D], lse [E,N,H_q]).
+
+    q [E,N,H_q,D] bf16: query j of stream e sees the prefix and its own rows
+    0 .. min(j, n_e - 1).  Other arguments as for ``attn_step``.
+    """
+    E, N, H_q, D = q.shape
+    H_kv = k_prefix.shape[1]
+    cap = k_event.shape[1]
+    if max_prefix_len is None:
+        max_prefix_len = k_prefix.shape[0]
+    dims = make_dims(E, H_q, H_kv, D, cap, max_prefix_len, _dtype_code(q), scale, queries_per_stream=N)
+    ws_bytes = workspace_size(dims, 1)
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None:
+        lse = torch.empty((E, N, H_q), dtype=torch.float32, device=q.device)
+    if workspace is None:
+        workspace = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device=q.device)
+    if v_prefix.shape != k_prefix.shape or v_event.shape != k_event.shape or k_event.shape[0] != E:
+        raise ValueError("inconsistent K/V shapes")
+    if event_lens.shape[0] != E or out.shape != q.shape or lse.shape != (E, N, H_q):
+        raise ValueError("event_lens / out / lse shape")
+    args = [_dev(q, "q", ndim=4), _dev(k_prefix, "k_prefix", q.dtype, 3), _dev(v_prefix, "v_prefix", q.dtype, 3),
+            _dev(k_event, "k_event", q.dtype, 4), _dev(v_event, "v_event", q.dtype, 4),
+            _dev(event_lens, "event_lens", torch.int32, 1), _dev(prefix_lens, "prefix_lens", torch.int32, 1),
+            _dev(out, "out", q.dtype, 4), _dev(lse, "lse", torch.float32, 3),
+            _dev(workspace, "workspace"), ctypes.c_size_t(workspace.numel() * workspace.element_size()),
+            _stream(stream, q.device)]
     _check("pdec_attn_step", lib().pdec_attn_step(ctypes.byref(dims), *args))
     return out, lse
 

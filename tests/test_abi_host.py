@@ -116,3 +116,21 @@ def test_step_rejects_bad_arguments_before_any_launch():
     assert L.pdec_attn_step_ragged(ctypes.byref(d), 1, *([good] * 3), None, *([good] * 3), None,
                                    good, good, good, ctypes.c_size_t(ws), None) == pdec.PDEC_ERR_INVALID_ARG
     assert L.pdec_kv_append(ctypes.byref(d), None, good, good, good, good, None, None) == pdec.PDEC_ERR_INVALID_ARG
+
+
+def test_whole_branches_need_bf16_without_plan_mask():
+    """queries_per_stream > 1 runs on the matrix-core kernel only, and not
+    together with the self-only plan mask; its workspace grows with it."""
+    one = pdec.make_dims(13, 28, 4, 128, 64, 32768, pdec.PDEC_DTYPE_BF16)
+    many = pdec.make_dims(13, 28, 4, 128, 64, 32768, pdec.PDEC_DTYPE_BF16, queries_per_stream=48)
+    assert pdec.workspace_size(many) > pdec.workspace_size(one) > 0
+    assert pdec.query_plan(many)[0] == pdec.PATH_MFMA
+    tiny = pdec.make_dims(1, 1, 1, 64, 4, 100, pdec.PDEC_DTYPE_BF16, queries_per_stream=2)
+    assert pdec.query_plan(tiny)[0] == pdec.PATH_MFMA  # 2 rows, still the matrix-core kernel
+    f32 = pdec.make_dims(13, 28, 4, 128, 64, 32768, pdec.PDEC_DTYPE_F32, queries_per_stream=48)
+    assert pdec.workspace_size(f32) == 0
+    plan = pdec.make_dims(13, 28, 4, 128, 64, 32768, pdec.PDEC_DTYPE_BF16, plan_mask=1, plan_per_stream=2,
+                          queries_per_stream=48)
+    assert pdec.workspace_size(plan) == 0
+    bad = pdec.make_dims(13, 28, 4, 128, 64, 32768, pdec.PDEC_DTYPE_BF16, queries_per_stream=-1)
+    assert pdec.workspace_size(bad) == 0

@@ -1,0 +1,95 @@
+"""Whole branches at once (queries_per_stream > 1; the prefill / training
+form of the §3.4 mask) on the GPU against the oracle's attn_prefill.
+
+Query j of stream e sees the prefix and its own rows 0 .. min(j, n_e - 1).
+Parity to the bf16 bar (max-abs 2e-2, normwise relative 1e-2 on out and
+lse), causality and blindness to other branches bitwise, and one query per
+stream bitwise equal to the decode step.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import check, dev_float, dev_int, host
+from paper_2607_02963_amd import pdec
+from paper_2607_02963_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+
+def _case(seed, E, N, L, lens, H_q=28, H_kv=4, D=128, cap=None, sigma=0.5):
+    rng = np.random.default_rng(seed)
+    cap = cap or N
+    f = lambda *shape: wl.bf16_bits((sigma * rng.standard_normal(shape)).astype(np.float32))  # noqa: E731
+    return dict(q=f(E, N, H_q, D), kp=f(L, H_kv, D), vp=f(L, H_kv, D), ke=f(E, cap, H_kv, D),
+                ve=f(E, cap, H_kv, D), n=np.asarray(lens, np.int32), L=L)
+
+
+def _run(c):
+    out, lse = pdec.attn_prefill(dev_float(c["q"], "bf16"), dev_float(c["kp"], "bf16"), dev_float(c["vp"], "bf16"),
+                                 dev_float(c["ke"], "bf16"), dev_float(c["ve"], "bf16"), dev_int(c["n"]),
+                                 dev_int([c["L"]]))
+    torch.cuda.synchronize()
+    return out, lse
+
+
+def _ref(c):
+    E = c["q"].shape[0]
+    return oracle.attn_prefill(c["q"], c["kp"], c["vp"], c["ke"], c["ve"], c["n"], [0, c["L"]], [0, E])
+
+
+CASES = [
+    # seed, E, N, L, lens, H_q, H_kv, D
+    (1, 3, 5, 700, [5, 3, 0], 28, 4, 128),
+    (2, 4, 16, 1000, [16, 16, 9, 1], 28, 4, 128),
+    (3, 6, 7, 515, [7, 7, 7, 7, 7, 7], 16, 2, 64),
+    (4, 1, 70, 300, [70], 8, 1, 128),
+    (5, 2, 3, 64, [3, 2], 4, 4, 64),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[f"E{c[1]}N{c[2]}L{c[3]}d{c[7]}" for c in CASES])
+def test_prefill_matches_oracle(case):
+    seed, E, N, L, lens, H_q, H_kv, D = case
+    c = _case(seed, E, N, L, lens, H_q, H_kv, D)
+    out, lse = _run(c)
+    ref_o, ref_l = _ref(c)
+    check("bf16", host(out).reshape(E * N, H_q, D), host(lse).reshape(E * N, H_q), ref_o.reshape(E * N, H_q, D),
+          ref_l.reshape(E * N, H_q), what=f"prefill case {seed}")
+
+
+def test_prefill_many_rows_medium_prefix():
+    """8 branches of 32 tokens over a 4096-token prefix: 1792 query rows per
+    kv head, several row groups per chunk."""
+    c = _case(6, 8, 32, 4096, [32, 32, 30, 17, 32, 1, 32, 25])
+    out, lse = _run(c)
+    ref_o, ref_l = _ref(c)
+    check("bf16", host(out).reshape(-1, 28, 128), host(lse).reshape(-1, 28), ref_o.reshape(-1, 28, 128),
+          ref_l.reshape(-1, 28), what="prefill 8x32 over 4096")
+
+
+def test_prefill_causal_and_blind_to_other_branches_bitwise():
+    c = _case(7, 4, 12, 800, [12, 12, 12, 12])
+    out, lse = _run(c)
+    d = dict(c)
+    ke, ve = c["ke"].copy(), c["ve"].copy()
+    big = wl.bf16_bits(np.full((8, 4, 128), 3e3, np.float32))
+    ke[1, 4:], ve[1, 4:] = big, big  # rows 4.. of branch 1
+    d["ke"], d["ve"] = ke, ve
+    out2, lse2 = _run(d)
+    assert torch.equal(out2[1, :4].view(torch.int16), out[1, :4].view(torch.int16))
+    assert torch.equal(lse2[1, :4], lse[1, :4])
+    keep = [0, 2, 3]
+    assert torch.equal(out2[keep].view(torch.int16), out[keep].view(torch.int16))
+    assert not torch.equal(out2[1, 4:], out[1, 4:])
+
+
+def test_one_query_per_stream_is_the_decode_step():
+    c = _case(8, 5, 1, 900, [1, 1, 0, 1, 1], cap=4)
+    out, lse = _run(c)
+    o2, l2 = pdec.attn_step(dev_float(np.ascontiguousarray(c["q"][:, 0]), "bf16"), dev_float(c["kp"], "bf16"),
+                            dev_float(c["vp"], "bf16"), dev_float(c["ke"], "bf16"), dev_float(c["ve"], "bf16"),
+                            dev_int(c["n"]), dev_int([c["L"]]))
+    torch.cuda.synchronize()
+    assert torch.equal(out[:, 0].view(torch.int16), o2.view(torch.int16)) and torch.equal(lse[:, 0], l2)
