@@ -66,7 +66,7 @@ def _load():
                            ctypes.c_void_p]
             fn = getattr(lib, f"oracle_attn_prefill_{sfx}")
             fn.restype = ctypes.c_int
-            fn.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p] + [ctypes.c_int] * 5 + \
+            fn.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p] + [ctypes.c_int] * 6 + \
                 [ctypes.c_double, ctypes.c_int] + [ctypes.c_void_p] * 8 + [ctypes.c_int]
             fn = getattr(lib, f"oracle_rope_append_{sfx}")
             fn.restype = ctypes.c_int
@@ -218,12 +218,13 @@ def rope_append(q, k_new, event_lens, live, cu_events=None, pos_base=None, cap=N
 
 
 def attn_prefill(q, k_prefix, v_prefix, k_event, v_event, event_lens, cu_prefix, cu_events, scale: float = 0.0,
-                 threads: int = 0, precision: str = "f64"):
+                 threads: int = 0, precision: str = "f64", cross: int = 0):
     """Event-factorized attention over whole branches (``oracle_attn_prefill``).
 
     q [SE, N, H_q, D]; other tensors as for ``attn_step``.  Query j of stream
-    e sees the prefix and its own rows 0 .. min(j, n_e - 1).  Returns
-    (out [SE, N, H_q, D], lse [SE, N, H_q]).
+    e sees the prefix and its own rows 0 .. min(j, n_e - 1); with ``cross``
+    (Table 8's "causal attention") also every other branch's rows t < j.
+    Returns (out [SE, N, H_q, D], lse [SE, N, H_q]).
     """
     lib = _load()
     real = np.float64 if precision == "f64" else np.float32
@@ -239,7 +240,8 @@ def attn_prefill(q, k_prefix, v_prefix, k_event, v_event, event_lens, cu_prefix,
     event_lens = _c(event_lens, np.int32)
     out = np.full((SE, N, H_q, D), np.nan, dtype=real)
     lse = np.full((SE, N, H_q), np.nan, dtype=real)
-    rc = fn(V, _ptr(cu_prefix), _ptr(cu_events), N, H_q, H_kv, D, cap, float(scale), dt, _ptr(q), _ptr(k_prefix),
+    rc = fn(V, _ptr(cu_prefix), _ptr(cu_events), N, int(cross), H_q, H_kv, D, cap, float(scale), dt, _ptr(q),
+            _ptr(k_prefix),
             _ptr(v_prefix), _ptr(k_event), _ptr(v_event), _ptr(event_lens), _ptr(out), _ptr(lse), int(threads))
     if rc != 0:
         raise ValueError("oracle_attn_prefill rejected its arguments")

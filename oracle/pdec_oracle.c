@@ -99,7 +99,11 @@ static real load_elem(const void* base, size_t idx, int dtype)
  * stream e only if it lies in e's own run of plan_T tokens.  The plan segment
  * must fit in the prefix (E*plan_T <= L).
  */
-int ORACLE_FN(oracle_build_mask)(int L, int E, int cap, const int32_t* n, int plan_mask, int plan_T, uint8_t* mask)
+/* cross_limit > 0 (the "causal attention" row of Table 8, whole branches
+ * only): row t of another stream f is also visible when t < cross_limit,
+ * i.e. when its position comes before the query's. */
+static int build_mask_x(int L, int E, int cap, const int32_t* n, int plan_mask, int plan_T, int cross_limit,
+                        uint8_t* mask)
 {
     if (L < 0 || E < 0 || cap < 0 || plan_T < 0 || (!mask && E > 0)) return -1;
     const long plan0 = (plan_mask && plan_T > 0) ? (long)L - (long)E * plan_T : (long)L;
@@ -114,8 +118,16 @@ int ORACLE_FN(oracle_build_mask)(int L, int E, int cap, const int32_t* n, int pl
         for (int f = 0; f < E; ++f)
             for (int t = 0; t < cap; ++t)
                 if (f == e && t < n[e]) row[L + (long)f * cap + t] = 1; /* own stream only */
+        for (int f = 0; f < E; ++f)                                            /* causal across streams */
+            for (int t = 0; t < cap; ++t)
+                if (f != e && t < n[f] && t < cross_limit) row[L + (long)f * cap + t] = 1;
     }
     return 0;
+}
+
+int ORACLE_FN(oracle_build_mask)(int L, int E, int cap, const int32_t* n, int plan_mask, int plan_T, uint8_t* mask)
+{
+    return build_mask_x(L, E, cap, n, plan_mask, plan_T, 0, mask);
 }
 
 /*
@@ -144,12 +156,11 @@ int ORACLE_FN(oracle_build_mask)(int L, int E, int cap, const int32_t* n, int pl
  *   num_threads           0 = OpenMP default
  * Returns 0, or -1 on inconsistent arguments.
  */
-int ORACLE_FN(oracle_attn_step)(int num_videos, const int32_t* cu_prefix, const int32_t* cu_events,
-                                int H_q, int H_kv, int D, int cap, double scale, int dtype,
-                                int plan_mask, int plan_T, const void* q, const void* k_prefix, const void* v_prefix,
-                                const void* k_event, const void* v_event, const int32_t* n,
-                                const uint8_t* row_select, real* out, real* lse, real* probs,
-                                int num_threads)
+static int attn_step_x(int num_videos, const int32_t* cu_prefix, const int32_t* cu_events, int H_q, int H_kv,
+                       int D, int cap, double scale, int dtype, int plan_mask, int plan_T, int cross_limit,
+                       const void* q, const void* k_prefix, const void* v_prefix, const void* k_event,
+                       const void* v_event, const int32_t* n, const uint8_t* row_select, real* out, real* lse,
+                       real* probs, int num_threads)
 {
     if (num_videos < 0 || H_q <= 0 || H_kv <= 0 || H_q % H_kv != 0 || D <= 0 || cap < 0) return -1;
     if (probs && num_videos != 1) return -1;
@@ -170,7 +181,7 @@ int ORACLE_FN(oracle_attn_step)(int num_videos, const int32_t* cu_prefix, const 
         const long U = (long)L + (long)E * cap;
         uint8_t* mask = (uint8_t*)malloc((size_t)(E > 0 ? E : 1) * (size_t)(U > 0 ? U : 1));
         if (!mask) return -1;
-        if (ORACLE_FN(oracle_build_mask)(L, E, cap, n + e0, plan_mask, plan_T, mask) != 0) {
+        if (build_mask_x(L, E, cap, n + e0, plan_mask, plan_T, cross_limit, mask) != 0) {
             free(mask);
             return -1;
         }
@@ -241,6 +252,17 @@ int ORACLE_FN(oracle_attn_step)(int num_videos, const int32_t* cu_prefix, const 
     return 0;
 }
 
+int ORACLE_FN(oracle_attn_step)(int num_videos, const int32_t* cu_prefix, const int32_t* cu_events,
+                                int H_q, int H_kv, int D, int cap, double scale, int dtype,
+                                int plan_mask, int plan_T, const void* q, const void* k_prefix, const void* v_prefix,
+                                const void* k_event, const void* v_event, const int32_t* n,
+                                const uint8_t* row_select, real* out, real* lse, real* probs,
+                                int num_threads)
+{
+    return attn_step_x(num_videos, cu_prefix, cu_events, H_q, H_kv, D, cap, scale, dtype, plan_mask, plan_T, 0, q,
+                       k_prefix, v_prefix, k_event, v_event, n, row_select, out, lse, probs, num_threads);
+}
+
 /*
  * Event-parallel decode loop for one video (§3.4: all streams step together;
  * a stream that has emitted EOS stops independently and the others go on).
@@ -301,11 +323,15 @@ int ORACLE_FN(oracle_decode_loop)(int steps, int E, int H_q, int H_kv, int D, in
  * Query j of stream e is therefore the decode step of stream e holding
  * min(j + 1, n_e) rows, and the oracle evaluates exactly that, one step per
  * j.  A stream with n_e == 0 has no branch: its rows are 0 and -inf.
+ * cross != 0 selects the "causal attention" row of Table 8 instead: the
+ * tokens of one decoding step share a position (§3.4), and ordinary causal
+ * attention then also shows query j every other branch's rows at earlier
+ * positions, t < j (and t < n_f).
  *   q [SE, N, H_q, D];  out [SE, N, H_q, D], lse [SE, N, H_q]  (real);
  *   other arguments as for oracle_attn_step (no plan mask).
  */
 int ORACLE_FN(oracle_attn_prefill)(int num_videos, const int32_t* cu_prefix, const int32_t* cu_events, int N,
-                                   int H_q, int H_kv, int D, int cap, double scale, int dtype, const void* q,
+                                   int cross, int H_q, int H_kv, int D, int cap, double scale, int dtype, const void* q,
                                    const void* k_prefix, const void* v_prefix, const void* k_event,
                                    const void* v_event, const int32_t* n, real* out, real* lse, int num_threads)
 {
@@ -323,9 +349,8 @@ int ORACLE_FN(oracle_attn_prefill)(int num_videos, const int32_t* cu_prefix, con
             memcpy(qj + (size_t)e * qrow, (const unsigned char*)q + ((size_t)e * N + j) * qrow, qrow);
             nj[e] = n[e] <= 0 ? 0 : (j + 1 < n[e] ? j + 1 : n[e]);
         }
-        rc = ORACLE_FN(oracle_attn_step)(num_videos, cu_prefix, cu_events, H_q, H_kv, D, cap, scale, dtype, 0, 0,
-                                         qj, k_prefix, v_prefix, k_event, v_event, nj, NULL, oj, lj, NULL,
-                                         num_threads);
+        rc = attn_step_x(num_videos, cu_prefix, cu_events, H_q, H_kv, D, cap, scale, dtype, 0, 0, cross ? j : 0, qj,
+                         k_prefix, v_prefix, k_event, v_event, nj, NULL, oj, lj, NULL, num_threads);
         for (int e = 0; e < SE && rc == 0; ++e) {
             memcpy(out + ((size_t)e * N + j) * H_q * D, oj + (size_t)e * H_q * D, (size_t)H_q * D * sizeof(real));
             memcpy(lse + ((size_t)e * N + j) * H_q, lj + (size_t)e * H_q, (size_t)H_q * sizeof(real));

@@ -39,6 +39,9 @@ MUTANTS = {
     "prefill_row_off_by_one": ("(j + 1 < n[e] ? j + 1 : n[e])", "(j < n[e] ? j : n[e])"),
     "prefill_not_causal": ("(j + 1 < n[e] ? j + 1 : n[e])", "n[e]"),
     "prefill_wrong_token": ("((size_t)e * N + j) * qrow, qrow);", "((size_t)e * N + 0) * qrow, qrow);"),
+    "cross_same_position_visible": ("t < n[f] && t < cross_limit)", "t < n[f] && t <= cross_limit)"),
+    "cross_ignored": ("cross ? j : 0, qj,", "0, qj,"),
+    "cross_past_branch_end": ("if (f != e && t < n[f] && t < cross_limit)", "if (f != e && t < cross_limit)"),
 }
 
 

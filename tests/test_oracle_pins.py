@@ -686,3 +686,42 @@ def test_prefill_query_equals_the_decode_step_at_that_token():
     o, l = oracle.attn_step(np.ascontiguousarray(q[:, j]), kp, vp, ke, ve, np.minimum(j + 1, n), [0, kp.shape[0]],
                             [0, 3])
     assert np.array_equal(out[:, j], o) and np.array_equal(lse[:, j], l)
+
+
+def test_causal_across_branches_zero_keys_average_the_earlier_rows():
+    """Table 8's "causal attention": the tokens of one step share a position
+    (§3.4), so query j also sees every other branch's rows at earlier
+    positions, t < j.  With all keys 0 the result is the plain mean of the
+    prefix, the own rows 0..j and the other branches' rows 0..j-1."""
+    q, kp, vp, ke, ve, n = _prefill_case(11, lens=(5, 3, 0))
+    kp[:] = 0
+    ke[:] = 0
+    out, lse = oracle.attn_prefill(q, kp, vp, ke, ve, n, [0, kp.shape[0]], [0, 3], cross=1)
+    G = q.shape[2] // kp.shape[1]
+    for e in range(3):
+        for j in range(q.shape[1]):
+            if n[e] == 0:
+                assert np.all(out[e, j] == 0) and np.all(np.isneginf(lse[e, j]))
+                continue
+            for h in range(q.shape[2]):
+                g = h // G
+                parts = [vp[:, g], ve[e, :min(j + 1, n[e]), g]]
+                parts += [ve[f, :min(j, n[f]), g] for f in range(3) if f != e]
+                rows = np.concatenate(parts).astype(np.float64)
+                np.testing.assert_allclose(out[e, j, h], rows.mean(axis=0), atol=1e-12)
+
+
+def test_causal_across_branches_sees_only_earlier_positions():
+    q, kp, vp, ke, ve, n = _prefill_case(12, lens=(5, 5, 5))
+    base, _ = oracle.attn_prefill(q, kp, vp, ke, ve, n, [0, kp.shape[0]], [0, 3], cross=1)
+    ke2, ve2 = ke.copy(), ve.copy()
+    ke2[1, 3:] += 4.0
+    ve2[1, 3:] -= 6.0
+    out, _ = oracle.attn_prefill(q, kp, vp, ke2, ve2, n, [0, kp.shape[0]], [0, 3], cross=1)
+    # queries 0..3 of the other branches see branch 1 only below row 3
+    assert np.array_equal(out[[0, 2], :4], base[[0, 2], :4])
+    assert not np.allclose(out[[0, 2], 4], base[[0, 2], 4])
+    # one branch: nothing else to see, the same as the factorized form
+    f1, _ = oracle.attn_prefill(q[:1], kp, vp, ke[:1], ve[:1], n[:1], [0, kp.shape[0]], [0, 1], cross=1)
+    f0, _ = oracle.attn_prefill(q[:1], kp, vp, ke[:1], ve[:1], n[:1], [0, kp.shape[0]], [0, 1])
+    assert np.array_equal(f0, f1)
