@@ -91,6 +91,10 @@ typedef struct pdec_dims {
                                   /* prefix and its own rows 0 .. min(j, n_e - 1), never another  */
                                   /* stream's; n_e == 0 gives rows of 0 / -inf.  Q > 1 needs      */
                                   /* bfloat16 and plan_mask == 0 (else PDEC_ERR_UNSUPPORTED).    */
+    int32_t cross_causal;         /* 0: the event-factorized mask.  1: the "causal attention" row */
+                                  /* of Table 8 (whole branches only, queries_per_stream > 1):   */
+                                  /* the tokens of one step share a position (§3.4), so query j */
+                                  /* also sees every other stream's rows t < min(j, n_f).        */
 } pdec_dims;
 
 /* Human-readable text of a pdec_status code.  Never NULL. */

@@ -289,9 +289,16 @@ __global__ __launch_bounds__(512) void split_mfma_kernel(StepArgs a)
                         const bool kout = kb + 16 * kt + 4 * lg + i >= ui.nk;
 #pragma unroll
                         for (int nt = 0; nt < NT; ++nt) {
-                            bool hide = kout || (ui.stream >= 0 && lane_stream[nt] != ui.stream);
-                            // whole branches: query j sees its own rows 0 .. j only
-                            if constexpr (MQ) hide = hide || (ui.stream >= 0 && ui.k0 + kb + 16 * kt + 4 * lg + i > lane_tok[nt]);
+                            bool hide;
+                            if constexpr (MQ) {
+                                // whole branches: query j sees its own rows 0 .. j; with the
+                                // causal-attention variant also other streams' rows 0 .. j-1
+                                const bool other = lane_stream[nt] != ui.stream;
+                                const int lim = other ? (a.cross ? lane_tok[nt] - 1 : -1) : lane_tok[nt];
+                                hide = kout || (ui.stream >= 0 && ui.k0 + kb + 16 * kt + 4 * lg + i > lim);
+                            } else {
+                                hide = kout || (ui.stream >= 0 && lane_stream[nt] != ui.stream);
+                            }
                             if (hide) s[kt][nt][i] = kNegInf;
                         }
                     }
@@ -360,7 +367,7 @@ __global__ __launch_bounds__(512) void split_mfma_kernel(StepArgs a)
         const UnitInfo ui = unit_info(a, vi, upre, tab_start, tab_nlen, id.g, u0 + st);
         // an own unit of stream f only concerns the rows of f
         bool wave_has_rows = row_wave_active;
-        if (ui.stream >= 0) {
+        if (ui.stream >= 0 && !(MQ && a.cross)) {
             const int f0 = ui.stream * a.G * a.qps, f1 = f0 + a.G * a.qps;  // video rows of stream f
             wave_has_rows = wave_has_rows && f0 < wrow0 + 16 * NT && f1 > wrow0;
         }

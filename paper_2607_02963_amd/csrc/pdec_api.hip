@@ -73,6 +73,8 @@ int validate_dims(const pdec_dims* d, int num_videos)
         d->max_events_per_video < 0 || d->max_events_per_video > d->num_events || d->prefix_tokens < 0 ||
         d->plan_mask < 0 || d->plan_mask > 1 || d->plan_tokens_per_stream < 0 || d->queries_per_stream < 0)
         return PDEC_ERR_INVALID_ARG;
+    if (d->cross_causal < 0 || d->cross_causal > 1) return PDEC_ERR_INVALID_ARG;
+    if (d->cross_causal && d->queries_per_stream <= 1) return PDEC_ERR_UNSUPPORTED;
     // whole branches run on the matrix-core kernel only, without the plan mask
     if (d->queries_per_stream > 1 &&
         (d->dtype != PDEC_DTYPE_BF16 || (d->plan_mask && d->plan_tokens_per_stream > 0)))
@@ -227,6 +229,7 @@ int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_pr
     a.qscale = scale * 1.4426950408889634f;
     a.plan_T = d->plan_mask ? d->plan_tokens_per_stream : 0;
     a.qps = std::max(d->queries_per_stream, 1);
+    a.cross = d->cross_causal;
 
     hipStream_t s = static_cast<hipStream_t>(stream);
     const int grid = 8 * a.items_per_xcd;

@@ -61,6 +61,7 @@ struct StepArgs {
     float qscale;               // softmax scale * log2(e)
     int plan_T;                 // plan tokens per stream when the self-only plan mask is on, else 0
     int qps;                    // queries per stream: 1 for a decode step, N for whole branches
+    int cross;                  // whole branches: other streams' rows at earlier positions visible
 };
 
 // Launch of the matrix-core split pass (its own translation unit).

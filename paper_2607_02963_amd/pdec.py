@@ -39,7 +39,7 @@ class Dims(ctypes.Structure):
                 ("max_events_per_video", ctypes.c_int32), ("dtype", ctypes.c_int32),
                 ("softmax_scale", ctypes.c_float), ("prefix_tokens", ctypes.c_int64),
                 ("plan_mask", ctypes.c_int32), ("plan_tokens_per_stream", ctypes.c_int32),
-                ("queries_per_stream", ctypes.c_int32)]
+                ("queries_per_stream", ctypes.c_int32), ("cross_causal", ctypes.c_int32)]
 
 
 class GroundDims(ctypes.Structure):
@@ -137,10 +137,10 @@ def _stream(stream, device) -> ctypes.c_void_p:
 
 def make_dims(num_events, H_q, H_kv, D, cap, max_prefix_len, dtype_code, scale=0.0,
               max_events_per_video=0, prefix_tokens=0, plan_mask=0, plan_per_stream=0,
-              queries_per_stream=0) -> Dims:
+              queries_per_stream=0, cross_causal=0) -> Dims:
     return Dims(int(num_events), int(H_q), int(H_kv), int(D), int(cap), int(max_prefix_len),
                 int(max_events_per_video), int(dtype_code), float(scale), int(prefix_tokens), int(plan_mask),
-                int(plan_per_stream), int(queries_per_stream))
+                int(plan_per_stream), int(queries_per_stream), int(cross_causal))
 
 
 def workspace_size(dims: Dims, num_videos: int = 1) -> int:
@@ -210,19 +210,22 @@ def attn_step(q, k_prefix, v_prefix, k_event, v_event, event_lens, prefix_lens, 
 
 
 def attn_prefill(q, k_prefix, v_prefix, k_event, v_event, event_lens, prefix_lens, *, out=None, lse=None,
-                 workspace=None, max_prefix_len=None, scale=0.0, stream=None):
+                 workspace=None, max_prefix_len=None, scale=0.0, stream=None, cross=0):
     """Whole branches of one video at once (``queries_per_stream`` N in
     pdec_dims); returns (out [E,N,H_q,D], lse [E,N,H_q]).
 
     q [E,N,H_q,D] bf16: query j of stream e sees the prefix and its own rows
-    0 .. min(j, n_e - 1).  Other arguments as for ``attn_step``.
+    0 .. min(j, n_e - 1); with ``cross`` 1 (Table 8's causal attention) also
+    every other stream's rows t < min(j, n_f).  Other arguments as for
+    ``attn_step``.
     """
     E, N, H_q, D = q.shape
     H_kv = k_prefix.shape[1]
     cap = k_event.shape[1]
     if max_prefix_len is None:
         max_prefix_len = k_prefix.shape[0]
-    dims = make_dims(E, H_q, H_kv, D, cap, max_prefix_len, _dtype_code(q), scale, queries_per_stream=N)
+    dims = make_dims(E, H_q, H_kv, D, cap, max_prefix_len, _dtype_code(q), scale, queries_per_stream=N,
+                     cross_causal=cross)
     ws_bytes = workspace_size(dims, 1)
     if out is None:
         out = torch.empty_like(q)

@@ -26,17 +26,17 @@ def _case(seed, E, N, L, lens, H_q=28, H_kv=4, D=128, cap=None, sigma=0.5):
                 ve=f(E, cap, H_kv, D), n=np.asarray(lens, np.int32), L=L)
 
 
-def _run(c):
+def _run(c, cross=0):
     out, lse = pdec.attn_prefill(dev_float(c["q"], "bf16"), dev_float(c["kp"], "bf16"), dev_float(c["vp"], "bf16"),
                                  dev_float(c["ke"], "bf16"), dev_float(c["ve"], "bf16"), dev_int(c["n"]),
-                                 dev_int([c["L"]]))
+                                 dev_int([c["L"]]), cross=cross)
     torch.cuda.synchronize()
     return out, lse
 
 
-def _ref(c):
+def _ref(c, cross=0):
     E = c["q"].shape[0]
-    return oracle.attn_prefill(c["q"], c["kp"], c["vp"], c["ke"], c["ve"], c["n"], [0, c["L"]], [0, E])
+    return oracle.attn_prefill(c["q"], c["kp"], c["vp"], c["ke"], c["ve"], c["n"], [0, c["L"]], [0, E], cross=cross)
 
 
 CASES = [
@@ -93,3 +93,29 @@ def test_one_query_per_stream_is_the_decode_step():
                             dev_int(c["n"]), dev_int([c["L"]]))
     torch.cuda.synchronize()
     assert torch.equal(out[:, 0].view(torch.int16), o2.view(torch.int16)) and torch.equal(lse[:, 0], l2)
+
+
+@pytest.mark.parametrize("case", CASES[:4], ids=[f"E{c[1]}N{c[2]}L{c[3]}d{c[7]}" for c in CASES[:4]])
+def test_causal_across_branches_matches_oracle(case):
+    """Table 8's "causal attention" row: query j also sees the other
+    branches' rows at earlier positions."""
+    seed, E, N, L, lens, H_q, H_kv, D = case
+    c = _case(seed + 50, E, N, L, lens, H_q, H_kv, D)
+    out, lse = _run(c, cross=1)
+    ref_o, ref_l = _ref(c, cross=1)
+    check("bf16", host(out).reshape(E * N, H_q, D), host(lse).reshape(E * N, H_q), ref_o.reshape(E * N, H_q, D),
+          ref_l.reshape(E * N, H_q), what=f"causal prefill case {seed}")
+
+
+def test_causal_across_branches_sees_only_earlier_positions_bitwise():
+    c = _case(9, 4, 10, 600, [10, 10, 10, 10])
+    out, lse = _run(c, cross=1)
+    d = dict(c)
+    ke, ve = c["ke"].copy(), c["ve"].copy()
+    big = wl.bf16_bits(np.full((4, 4, 128), 2e3, np.float32))
+    ke[2, 6:], ve[2, 6:] = big, big  # rows 6.. of branch 2
+    d["ke"], d["ve"] = ke, ve
+    out2, _ = _run(d, cross=1)
+    others = [0, 1, 3]
+    assert torch.equal(out2[others, :7].view(torch.int16), out[others, :7].view(torch.int16))
+    assert not torch.equal(out2[others, 7:], out[others, 7:])
