@@ -304,22 +304,26 @@ __global__ __launch_bounds__(512) void split_mfma_kernel(StepArgs a)
                     }
             }
         }
-        // block max per row; rows whose max rose by more than 8 re-reference
-        float mt[NT];
+        // Rows whose block max rose by more than 8 re-reference.  The test
+        // takes each lane's own max: no lane above the threshold means no row
+        // above it, so the max over a row's four lane groups is formed only
+        // when some row may move (it is the same in all four groups, which
+        // keeps a row's reference identical across them).
+        float mx[NT];
         bool need = false;
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
-            const float mx = fmaxf(fmaxf(fmaxf(s[0][nt][0], s[0][nt][1]), fmaxf(s[0][nt][2], s[0][nt][3])),
-                                   fmaxf(fmaxf(s[1][nt][0], s[1][nt][1]), fmaxf(s[1][nt][2], s[1][nt][3])));
-            mt[nt] = max_over_groups(mx) * c;
-            need |= mt[nt] > m_ref[nt] + 8.f;
+            mx[nt] = fmaxf(fmaxf(fmaxf(s[0][nt][0], s[0][nt][1]), fmaxf(s[0][nt][2], s[0][nt][3])),
+                           fmaxf(fmaxf(s[1][nt][0], s[1][nt][1]), fmaxf(s[1][nt][2], s[1][nt][3])));
+            need |= mx[nt] * c > m_ref[nt] + 8.f;
         }
         if (__any(need)) {
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt) {
-                const bool up = mt[nt] > m_ref[nt] + 8.f;
-                const float alpha = up ? fast_exp2(m_ref[nt] - mt[nt]) : 1.f;
-                m_ref[nt] = up ? mt[nt] : m_ref[nt];
+                const float mt = max_over_groups(mx[nt]) * c;
+                const bool up = mt > m_ref[nt] + 8.f;
+                const float alpha = up ? fast_exp2(m_ref[nt] - mt) : 1.f;
+                m_ref[nt] = up ? mt : m_ref[nt];
                 lsum[nt] *= alpha;
 #pragma unroll
                 for (int dt = 0; dt < C::DT; ++dt) o[nt][dt] *= alpha;
