@@ -310,3 +310,82 @@ def grounding_32k(seed: int = 5) -> GroundingInputs:
     sizes = rng.integers(200, 311, size=128)
     sizes[-1] += 32704 - int(sizes.sum())
     return make_grounding(name="grounding_N32704_S128_K32", K=32, N=32704, S=128, d=256, seed=seed, sizes=sizes)
+
+
+@dataclass
+class AggregationInputs:
+    """Inputs of the aggregation into the event tokens: event token
+    embeddings g [K, hidden] and audio-visual token embeddings x [N, hidden]
+    (bf16 bit patterns), contiguous time segments cu_seg [S + 1], the
+    grounding's saliency salient [K, S] (uint8), the last text token's
+    queries q [H_q, D] and the audio-visual tokens' keys k [N, H_kv, D]
+    (bf16), that token's attention log-normalisers lse [H_q] (float32, drawn
+    as an input: in the model they come from the decode step over the whole
+    prefix) and learned importance scores [N] (float32)."""
+    name: str
+    g: np.ndarray
+    x: np.ndarray
+    cu_seg: np.ndarray
+    salient: np.ndarray
+    q: np.ndarray
+    k: np.ndarray
+    lse: np.ndarray
+    scores: np.ndarray
+    seed: int
+
+    @property
+    def K(self) -> int:
+        return self.g.shape[0]
+
+    @property
+    def N(self) -> int:
+        return self.x.shape[0]
+
+    @property
+    def S(self) -> int:
+        return self.cu_seg.shape[0] - 1
+
+    @property
+    def hidden(self) -> int:
+        return self.x.shape[1]
+
+
+def make_aggregation(*, name="aggregation", K=5, N=300, S=8, hidden=256, H_q=8, H_kv=2, D=64, seed=0, sizes=None,
+                     empty_events=1, max_run=8) -> AggregationInputs:
+    """Segment sizes are `sizes` when given (summing to N), else a random
+    split of N into S parts (some may be empty).  Each event is grounded to a
+    run of 1..max_run consecutive segments at a random place, as the
+    grounding's threshold on a well-trained event token gives; the last
+    `empty_events` events have no salient segment.  Query and key entries are
+    standard normal, so the scaled scores have unit spread."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    if sizes is None:
+        cuts = np.sort(rng.integers(0, N + 1, size=S - 1))
+        cu = np.concatenate([[0], cuts, [N]]).astype(np.int32)
+    else:
+        cu = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+        assert cu[-1] == N and cu.shape[0] == S + 1
+    g = bf16_bits(0.5 * rng.standard_normal((K, hidden), dtype=np.float32))
+    x = bf16_bits(0.5 * rng.standard_normal((N, hidden), dtype=np.float32))
+    sal = np.zeros((K, S), np.uint8)
+    for i in range(K - min(empty_events, K)):
+        run = int(rng.integers(1, min(max_run, S) + 1))
+        a = int(rng.integers(0, S - run + 1))
+        sal[i, a:a + run] = 1
+    q = bf16_bits(rng.standard_normal((H_q, D), dtype=np.float32))
+    k = bf16_bits(rng.standard_normal((N, H_kv, D), dtype=np.float32))
+    lse = (np.log(max(N, 1)) + 0.5 + rng.uniform(-0.5, 0.5, H_q)).astype(np.float32)
+    scores = rng.uniform(0.05, 1.0, N).astype(np.float32)
+    return AggregationInputs(name, g, x, cu, sal, q, k, lse, scores, seed)
+
+
+def aggregation_32k(seed: int = 6) -> AggregationInputs:
+    """The 32k prefix's audio-visual part (32704 tokens in 128 time segments
+    of about 255 tokens, as for the grounding workload), 32 event tokens,
+    token embeddings of width 3584 and the last text token's 28 query heads
+    over 4 kv heads of width 128 (the headline attention shape)."""
+    rng = np.random.Generator(np.random.PCG64(seed + 1000))
+    sizes = rng.integers(200, 311, size=128)
+    sizes[-1] += 32704 - int(sizes.sum())
+    return make_aggregation(name="aggregation_N32704_S128_K32_H3584", K=32, N=32704, S=128, hidden=3584, H_q=28,
+                            H_kv=4, D=128, seed=seed, sizes=sizes, empty_events=1)
