@@ -247,6 +247,64 @@ def run_rope(args, torch, pdec, wl):
     print(json.dumps(rec), flush=True)
 
 
+def run_aggregation(args, torch, pdec, wl):
+    """Attention-guided aggregation into the event tokens over the 32k
+    prefix's audio-visual tokens (32704 tokens with embeddings of width
+    3584 in 128 time segments, 32 event tokens, the last text token's 28
+    query heads over 4 kv heads of width 128; pdec_aggregate).  Inputs
+    rotate over copies totalling >= 512 MB so the 256 MB MALL cannot hold
+    them.  µs per call from HIP events around K back-to-back calls; the
+    algorithmic bytes are every input read once and the output written once
+    (the embeddings, 234 MB, dominate)."""
+    w = wl.aggregation_32k()
+
+    def f(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+
+    base = dict(g=f(w.g), x=f(w.x), cu=torch.from_numpy(w.cu_seg).cuda(), sal=torch.from_numpy(w.salient).cuda(),
+                q=f(w.q), k=f(w.k), lse=torch.from_numpy(w.lse).cuda())
+    set_bytes = sum(t.numel() * t.element_size() for t in base.values())
+    nsets = max(1, math.ceil(ROTATE_BYTES / set_bytes))
+    sets = [base] + [_clone_set(base) for _ in range(nsets - 1)]
+    H_q, D = w.q.shape
+    H_kv = w.k.shape[1]
+    out = torch.empty_like(base["g"])
+    ws = torch.empty(pdec.aggregation_workspace_size(w.K, w.N, w.S, w.hidden, "attention", H_q, H_kv, D),
+                     dtype=torch.uint8, device="cuda")
+
+    def call(i):
+        d = sets[i % nsets]
+        pdec.aggregate(d["g"], d["x"], d["cu"], d["sal"], "attention", q=d["q"], k=d["k"], lse=d["lse"], out=out,
+                       workspace=ws)
+
+    for i in range(args.warmup):
+        call(i)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(args.steps):
+        call(i)
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) / args.steps * 1e3
+    nbytes = (w.N * w.hidden * 2 + w.N * H_kv * D * 2 + 2 * w.K * w.hidden * 2 + H_q * D * 2 + H_q * 4
+              + (w.S + 1) * 4 + w.K * w.S)
+    gbps = nbytes / (us * 1e-6) / 1e9
+    _log(f"bench: aggregation {us:.2f} us/call, {nbytes / 1e6:.2f} MB, sets={nsets}")
+    rec = {
+        "metric": "us per attention-guided aggregation call (32 events, 32704 tokens of width 3584, 128 segments)",
+        "value": round(us, 3), "unit": "us/call", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "higher_is_better": False, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": w.name, "events": w.K, "tokens": w.N, "segments": w.S, "hidden": w.hidden,
+                   "H_q": H_q, "H_kv": H_kv, "head_dim": D, "mode": "attention", "seed": w.seed},
+        "roofline": {"bound": "hbm", "achieved": round(gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(gbps / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "kernel": "aggr_pool (with the attention weights) + aggr_segment + aggr_event (per call)",
+                     "kernel_us": round(us, 3), "kernel_algorithmic_bytes": nbytes},
+    }
+    print(json.dumps(rec), flush=True)
+
+
 def run_grounding(args, torch, pdec, wl):
     """Segment-level similarity grounding over the 32k prefix's audio-visual
     tokens (32704 tokens of width 256 after the projection, 128 time
@@ -357,7 +415,8 @@ def main():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="long_32k",
-                    help="long_32k | single_8k | ragged_16 | tiny_f32 | loop_64 | rope_append | grounding | prefill")
+                    help="long_32k | single_8k | ragged_16 | tiny_f32 | loop_64 | rope_append | grounding | prefill"
+                         " | aggregation")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--plan-mask", choices=("full", "self"), default="full",
                     help="full: every stream sees all plan tokens (the full design); self: each stream sees only "
@@ -396,6 +455,9 @@ def main():
         return
     if args.workload == "grounding":
         run_grounding(args, torch, pdec, wl)
+        return
+    if args.workload == "aggregation":
+        run_aggregation(args, torch, pdec, wl)
         return
     if args.workload == "prefill":
         run_prefill(args, torch, pdec, wl)

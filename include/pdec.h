@@ -254,6 +254,67 @@ int pdec_segment_grounding(const pdec_ground_dims* dims, const void* g, const vo
                            float threshold, float* scores, uint8_t* salient, void* workspace,
                            size_t workspace_bytes, void* stream);
 
+/*
+ * Adaptive semantic aggregation into the global event tokens (§3.3,
+ * "Adaptive Semantic Aggregation", strategies (1)-(3)).  For the K event
+ * token embeddings g_i of a video and its N audio-visual prefix token
+ * embeddings x_n, with the salient segments of each event (the output of
+ * pdec_segment_grounding):
+ *   out_i = g_i + sum_{n in sel_i} w_n x_n / sum_{n in sel_i} w_n,
+ * sel_i the tokens of event i's salient segments; out_i = g_i when sel_i is
+ * empty or its weights sum to 0.  The token weights are
+ *   PDEC_AGGR_UNIFORM    w_n = 1 (mean pooling);
+ *   PDEC_AGGR_LEARNED    w_n = scores[n] (the caller's scoring head);
+ *   PDEC_AGGR_ATTENTION  the attention weights of the last text query token
+ *                        over the tokens, averaged over its query heads:
+ *                        w_n = (1/H_q) sum_h exp(scale <q_h, k[n, h / (H_q/H_kv)]> - lse[h]),
+ *                        lse the log-normalisers of that token's attention rows
+ *                        (the decode step's lse output for it).
+ * Segments, clamping and determinism as for pdec_segment_grounding: sums run
+ * in float32 in a fixed order (per 64-token chunk, per segment, per event),
+ * and each output element is rounded once to bf16.
+ */
+enum { PDEC_AGGR_UNIFORM = 0, PDEC_AGGR_LEARNED = 1, PDEC_AGGR_ATTENTION = 2 };
+
+typedef struct pdec_aggr_dims {
+    int32_t num_events;    /* K >= 1                                                   */
+    int32_t num_tokens;    /* N >= 1                                                   */
+    int32_t num_segments;  /* S >= 1                                                   */
+    int32_t hidden;        /* embedding width: a multiple of 8, at most 8192           */
+    int32_t mode;          /* PDEC_AGGR_UNIFORM, PDEC_AGGR_LEARNED or PDEC_AGGR_ATTENTION */
+    int32_t num_q_heads;   /* attention mode: H_q, 1..64, a multiple of num_kv_heads   */
+    int32_t num_kv_heads;  /* attention mode: H_kv, divides num_q_heads                */
+    int32_t head_dim;      /* attention mode: 64 or 128                                */
+    float softmax_scale;   /* attention mode: 0 means 1/sqrt(head_dim)                 */
+    int32_t dtype;         /* PDEC_DTYPE_BF16 (the only type with a kernel)            */
+} pdec_aggr_dims;
+
+/* Workspace bytes for pdec_aggregate (0 for invalid dims).  Host only. */
+size_t pdec_aggregation_workspace_size(const pdec_aggr_dims* dims);
+
+/*
+ *   g [K, hidden], x [N, hidden]   device, bf16, rows contiguous, 16-byte aligned;
+ *   cu_seg [S + 1] int32           device, non-decreasing from 0 to N (not checked:
+ *                                  ranges are clamped to [0, N), so a bad table gives
+ *                                  wrong sums, never a stray access);
+ *   salient [K, S] uint8           device, nonzero = salient;
+ *   scores [N] float32             device, learned mode only (else ignored, may be NULL);
+ *   q [H_q, D], k [N, H_kv, D]     device, bf16, 16-byte aligned, attention mode only:
+ *                                  the last text token's queries and the audio-visual
+ *                                  tokens' keys (a contiguous slice of the prefix cache);
+ *   lse [H_q] float32              device, attention mode only;
+ *   weights [N] float32            device, attention mode: if not NULL, receives the
+ *                                  token weights w_n; ignored in the other modes;
+ *   out [K, hidden] bf16           device, written; may be g itself (in place);
+ *   workspace >= pdec_aggregation_workspace_size(dims) bytes, device, 256-byte
+ *                                  aligned, contents ignored.
+ * Asynchronous on `stream` (three launches).
+ * Returns a pdec_status.
+ */
+int pdec_aggregate(const pdec_aggr_dims* dims, const void* g, const void* x, const int32_t* cu_seg,
+                   const uint8_t* salient, const float* scores, const void* q, const void* k, const float* lse,
+                   float* weights, void* out, void* workspace, size_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

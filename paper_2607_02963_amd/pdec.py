@@ -27,7 +27,10 @@ PATH_AUTO, PATH_VALU, PATH_MFMA = 0, 1, 2
 
 EXPORTED = ("pdec_strerror", "pdec_workspace_size", "pdec_attn_step", "pdec_attn_step_ragged",
             "pdec_kv_append", "pdec_rope_kv_append", "pdec_set_path", "pdec_query_plan",
-            "pdec_set_split_timer", "pdec_grounding_workspace_size", "pdec_segment_grounding")
+            "pdec_set_split_timer", "pdec_grounding_workspace_size", "pdec_segment_grounding",
+            "pdec_aggregation_workspace_size", "pdec_aggregate")
+
+AGGR_MODES = {"uniform": 0, "learned": 1, "attention": 2}
 
 
 class Dims(ctypes.Structure):
@@ -47,6 +50,15 @@ class GroundDims(ctypes.Structure):
 
     _fields_ = [("num_events", ctypes.c_int32), ("num_tokens", ctypes.c_int32),
                 ("num_segments", ctypes.c_int32), ("dim", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+class AggrDims(ctypes.Structure):
+    """Mirror of ``pdec_aggr_dims``."""
+
+    _fields_ = [("num_events", ctypes.c_int32), ("num_tokens", ctypes.c_int32),
+                ("num_segments", ctypes.c_int32), ("hidden", ctypes.c_int32), ("mode", ctypes.c_int32),
+                ("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("softmax_scale", ctypes.c_float), ("dtype", ctypes.c_int32)]
 
 
 class PdecError(RuntimeError):
@@ -89,6 +101,11 @@ def lib():
         L.pdec_grounding_workspace_size.argtypes = [gp]
         L.pdec_segment_grounding.restype = ctypes.c_int
         L.pdec_segment_grounding.argtypes = [gp, vp, vp, vp, ctypes.c_float, vp, vp, vp, sz, vp]
+        ap = ctypes.POINTER(AggrDims)
+        L.pdec_aggregation_workspace_size.restype = ctypes.c_size_t
+        L.pdec_aggregation_workspace_size.argtypes = [ap]
+        L.pdec_aggregate.restype = ctypes.c_int
+        L.pdec_aggregate.argtypes = [ap, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         L.pdec_set_path.restype = ctypes.c_int
         L.pdec_set_path.argtypes = [ctypes.c_int]
         L.pdec_query_plan.restype = ctypes.c_int
@@ -350,6 +367,59 @@ def segment_grounding(g, p, cu_seg, threshold, *, scores=None, salient=None, wor
             ctypes.c_size_t(workspace.numel() * workspace.element_size()), _stream(stream, g.device)]
     _check("pdec_segment_grounding", lib().pdec_segment_grounding(ctypes.byref(dims), *args))
     return scores, salient
+
+
+def aggr_dims(K, N, S, hidden, mode, H_q=0, H_kv=0, D=0, scale=0.0, dtype_code=PDEC_DTYPE_BF16) -> AggrDims:
+    return AggrDims(int(K), int(N), int(S), int(hidden), AGGR_MODES[mode] if isinstance(mode, str) else int(mode),
+                    int(H_q), int(H_kv), int(D), float(scale), int(dtype_code))
+
+
+def aggregation_workspace_size(K, N, S, hidden, mode, H_q=0, H_kv=0, D=0) -> int:
+    return int(lib().pdec_aggregation_workspace_size(ctypes.byref(aggr_dims(K, N, S, hidden, mode, H_q, H_kv, D))))
+
+
+def aggregate(g, x, cu_seg, salient, mode, *, scores=None, q=None, k=None, lse=None, weights=None, out=None,
+              scale=0.0, workspace=None, stream=None):
+    """Aggregation of the salient tokens into the event tokens (``pdec_aggregate``).
+
+    g [K,hidden], x [N,hidden] bf16; cu_seg int32 [S+1]; salient uint8 [K,S];
+    mode "uniform", "learned" (scores float32 [N]) or "attention" (q [H_q,D],
+    k [N,H_kv,D] bf16, lse float32 [H_q]; ``weights`` float32 [N] receives the
+    token weights when given).  Returns out [K,hidden] bf16 (``out`` may be g).
+    """
+    K, hidden = g.shape
+    N = x.shape[0]
+    S = cu_seg.shape[0] - 1
+    if x.shape != (N, hidden) or salient.shape != (K, S):
+        raise ValueError("g, x and salient shapes disagree")
+    H_q = H_kv = D = 0
+    ptr = {"scores": None, "q": None, "k": None, "lse": None, "weights": None}
+    if mode == "learned":
+        ptr["scores"] = _dev(scores, "scores", torch.float32, 1)
+    elif mode == "attention":
+        H_q, D = q.shape
+        H_kv = k.shape[1]
+        if k.shape != (N, H_kv, D):
+            raise ValueError("k must be [N, H_kv, D]")
+        ptr["q"] = _dev(q, "q", g.dtype, 2)
+        ptr["k"] = _dev(k, "k", g.dtype, 3)
+        ptr["lse"] = _dev(lse, "lse", torch.float32, 1)
+        if weights is not None:
+            ptr["weights"] = _dev(weights, "weights", torch.float32, 1)
+    elif mode != "uniform":
+        raise ValueError(f"unknown mode {mode!r}")
+    dims = aggr_dims(K, N, S, hidden, mode, H_q, H_kv, D, scale, _dtype_code(g))
+    if out is None:
+        out = torch.empty_like(g)
+    ws_bytes = int(lib().pdec_aggregation_workspace_size(ctypes.byref(dims)))
+    if workspace is None:
+        workspace = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=g.device)
+    args = [_dev(g, "g", None, 2), _dev(x, "x", g.dtype, 2), _dev(cu_seg, "cu_seg", torch.int32, 1),
+            _dev(salient, "salient", torch.uint8, 2), ptr["scores"], ptr["q"], ptr["k"], ptr["lse"],
+            ptr["weights"], _dev(out, "out", g.dtype, 2), ctypes.c_void_p(workspace.data_ptr()),
+            ctypes.c_size_t(workspace.numel() * workspace.element_size()), _stream(stream, g.device)]
+    _check("pdec_aggregate", lib().pdec_aggregate(ctypes.byref(dims), *args))
+    return out
 
 
 class SplitTimer:

@@ -134,3 +134,42 @@ def test_whole_branches_need_bf16_without_plan_mask():
     assert pdec.workspace_size(plan) == 0
     bad = pdec.make_dims(13, 28, 4, 128, 64, 32768, pdec.PDEC_DTYPE_BF16, queries_per_stream=-1)
     assert pdec.workspace_size(bad) == 0
+
+
+def test_aggregation_workspace_and_dims_checks():
+    """Workspace size: the chunk pieces and the segment sums; 0 for dims the
+    library has no kernel for or that are invalid."""
+    K, N, S, hidden = 32, 32704, 128, 3584
+    size = pdec.aggregation_workspace_size(K, N, S, hidden, "attention", 28, 4, 128)
+    slots = (N + 63) // 64 + S
+    assert size >= 4 * (slots * hidden + slots + S * hidden + S)
+    assert pdec.aggregation_workspace_size(K, N, S, hidden, "uniform") == \
+        pdec.aggregation_workspace_size(K, N, S, hidden, "learned")
+    bad = [(K, N, S, hidden + 4, "uniform", 0, 0, 0),        # width not a multiple of 8
+           (K, N, S, 8200, "uniform", 0, 0, 0),              # wider than 8192
+           (0, N, S, hidden, "uniform", 0, 0, 0),            # no events
+           (K, N, 0, hidden, "uniform", 0, 0, 0),            # no segments
+           (K, N, S, hidden, 3, 0, 0, 0),                    # unknown mode
+           (K, N, S, hidden, "attention", 28, 5, 128),       # H_q not a multiple of H_kv
+           (K, N, S, hidden, "attention", 28, 4, 96),        # head_dim
+           (K, N, S, hidden, "attention", 128, 4, 128)]      # more query heads than LDS holds
+    for args in bad:
+        assert pdec.aggregation_workspace_size(*args) == 0, args
+    d = pdec.aggr_dims(K, N, S, hidden, "uniform", dtype_code=pdec.PDEC_DTYPE_F32)
+    assert pdec.lib().pdec_aggregation_workspace_size(ctypes.byref(d)) == 0
+
+
+def test_aggregate_rejects_bad_arguments_before_any_launch():
+    d = pdec.aggr_dims(4, 100, 3, 64, "learned")
+    ws = ctypes.c_void_p(256)  # never dereferenced: the checks fail first
+    L = pdec.lib()
+    p = ctypes.c_void_p(4096)
+    # learned mode without scores
+    assert L.pdec_aggregate(ctypes.byref(d), p, p, p, p, None, None, None, None, None, p, ws,
+                            ctypes.c_size_t(1 << 30), None) == pdec.PDEC_ERR_INVALID_ARG
+    # misaligned embeddings
+    assert L.pdec_aggregate(ctypes.byref(d), ctypes.c_void_p(4098), p, p, p, p, None, None, None, None, p, ws,
+                            ctypes.c_size_t(1 << 30), None) == pdec.PDEC_ERR_INVALID_ARG
+    # workspace too small
+    assert L.pdec_aggregate(ctypes.byref(d), p, p, p, p, p, None, None, None, None, p, ws,
+                            ctypes.c_size_t(16), None) == pdec.PDEC_ERR_WORKSPACE
