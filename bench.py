@@ -409,6 +409,56 @@ def run_prefill(args, torch, pdec, wl):
     print(json.dumps(rec), flush=True)
 
 
+def run_prefix_causal(args, torch, pdec, wl):
+    """The prefix's own causal attention over 32768 tokens (H_q 28, H_kv 4,
+    D 128, bf16), run as whole branches: one stream, no shared prefix, the
+    prefix as its rows and one query per token.  A dense contraction:
+    algorithmic flops = 4 * D * H_q * sum over tokens j of (j + 1).  µs per
+    call from HIP events around K back-to-back calls."""
+    Q, H_q, H_kv, D = 32768, 28, 4, 128
+    rng = np.random.default_rng(7)
+
+    def f(*shape):
+        a = wl.bf16_bits((0.5 * rng.standard_normal(shape, dtype=np.float32)).astype(np.float32))
+        return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
+
+    q, ke, ve = f(1, Q, H_q, D), f(1, Q, H_kv, D), f(1, Q, H_kv, D)
+    empty = torch.empty((0, H_kv, D), dtype=torch.bfloat16, device="cuda")
+    lens = torch.full((1,), Q, dtype=torch.int32, device="cuda")
+    plen = torch.zeros((1,), dtype=torch.int32, device="cuda")
+    out = torch.empty_like(q)
+    lse = torch.empty((1, Q, H_q), dtype=torch.float32, device="cuda")
+    dims = pdec.make_dims(1, H_q, H_kv, D, Q, 0, pdec.PDEC_DTYPE_BF16, queries_per_stream=Q)
+    ws = torch.empty(pdec.workspace_size(dims), dtype=torch.uint8, device="cuda")
+
+    def call():
+        pdec.attn_prefill(q, empty, empty, ke, ve, lens, plen, out=out, lse=lse, workspace=ws)
+
+    for _ in range(args.warmup):
+        call()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        call()
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) / args.steps * 1e3
+    flops = 4 * D * H_q * (Q * (Q + 1) // 2)
+    tflops = flops / (us * 1e-6) / 1e12
+    _log(f"bench: prefix causal {us:.1f} us/call, {flops / 1e12:.2f} TFLOP, {tflops:.1f} TFLOP/s")
+    rec = {
+        "metric": "us per causal attention call over a 32768-token prefix (28 query heads, 4 kv heads)",
+        "value": round(us, 1), "unit": "us/call", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "higher_is_better": False, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "prefix_causal_L32768", "prefix_len": Q, "H_q": H_q, "H_kv": H_kv, "head_dim": D},
+        "roofline": {"bound": "mfma", "achieved": round(tflops, 1), "peak": 2500.0, "unit": "TFLOP/s",
+                     "frac": round(tflops / 2500.0, 4), "traffic": None, "kernel": "split pass + finish (per call)",
+                     "kernel_us": round(us, 1), "kernel_algorithmic_flops": flops},
+    }
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -416,7 +466,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="long_32k",
                     help="long_32k | single_8k | ragged_16 | tiny_f32 | loop_64 | rope_append | grounding | prefill"
-                         " | aggregation")
+                         " | aggregation | prefix_causal")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--plan-mask", choices=("full", "self"), default="full",
                     help="full: every stream sees all plan tokens (the full design); self: each stream sees only "
@@ -455,6 +505,9 @@ def main():
         return
     if args.workload == "grounding":
         run_grounding(args, torch, pdec, wl)
+        return
+    if args.workload == "prefix_causal":
+        run_prefix_causal(args, torch, pdec, wl)
         return
     if args.workload == "aggregation":
         run_aggregation(args, torch, pdec, wl)

@@ -158,7 +158,19 @@ __global__ __launch_bounds__(512) void split_mfma_kernel(StepArgs a)
         u1 = min(u1, total);
     }
     if (u0 >= u1) return;
-    const int nstages = u1 - u0;
+    int nstages = u1 - u0;
+    if constexpr (MQ) {
+        // whole branches: rows of one stream f see none of the units after
+        // f's unit holding their largest token (other streams' units are
+        // hidden without the causal-attention variant).  The item still
+        // writes its partial state, empty if no stage is left.
+        const int per = a.G * a.qps;
+        const int f = row0 / per;
+        if (!a.cross && (row0 + nrows - 1) / per == f && u1 > upre) {
+            const int tok_hi = ((row0 + nrows - 1) / a.G) % a.qps;
+            nstages = max(0, min(nstages, upre + tab_start[f] + tok_hi / kUnit + 1 - u0));
+        }
+    }
 
     const uint16_t* __restrict__ kpre = static_cast<const uint16_t*>(a.k_prefix);
     const uint16_t* __restrict__ vpre = static_cast<const uint16_t*>(a.v_prefix);
@@ -190,6 +202,34 @@ __global__ __launch_bounds__(512) void split_mfma_kernel(StepArgs a)
         }
     }
     wait_vmcnt<0>();
+
+    // Whole branches: the range of query tokens and streams among this
+    // wave's rows (uniform over the wave).  No row sees an own key above the
+    // largest token, and an own unit that lies below the smallest token of a
+    // wave whose rows all belong to its stream is seen whole by every row.
+    int w_tok_lo = 0x7fffffff, w_tok_hi = -1, w_str_lo = 0x7fffffff, w_str_hi = -1;
+    if constexpr (MQ) {
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+            if (lane_stream[nt] >= 0) {
+                w_tok_lo = min(w_tok_lo, lane_tok[nt]);
+                w_tok_hi = max(w_tok_hi, lane_tok[nt]);
+                w_str_lo = min(w_str_lo, lane_stream[nt]);
+                w_str_hi = max(w_str_hi, lane_stream[nt]);
+            }
+        }
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) {
+            w_tok_lo = min(w_tok_lo, __shfl_xor(w_tok_lo, off));
+            w_tok_hi = max(w_tok_hi, __shfl_xor(w_tok_hi, off));
+            w_str_lo = min(w_str_lo, __shfl_xor(w_str_lo, off));
+            w_str_hi = max(w_str_hi, __shfl_xor(w_str_hi, off));
+        }
+        w_tok_lo = __builtin_amdgcn_readfirstlane(w_tok_lo);
+        w_tok_hi = __builtin_amdgcn_readfirstlane(w_tok_hi);
+        w_str_lo = __builtin_amdgcn_readfirstlane(w_str_lo);
+        w_str_hi = __builtin_amdgcn_readfirstlane(w_str_hi);
+    }
 
     // DMA of one stage (unit u0 + st): this wave's DMA_PER_WAVE 1 KB pieces.
     // Piece p covers KPI keys of K (p < DMA_PER_STAGE/2) or of V; lane l
@@ -375,10 +415,19 @@ __global__ __launch_bounds__(512) void split_mfma_kernel(StepArgs a)
             const int f0 = ui.stream * a.G * a.qps, f1 = f0 + a.G * a.qps;  // video rows of stream f
             wave_has_rows = wave_has_rows && f0 < wrow0 + 16 * NT && f1 > wrow0;
         }
+        bool whole = ui.stream < 0 && ui.nk == kUnit && (!PLAN || ui.k0 + kUnit <= vi.plan0);
+        if constexpr (MQ) {
+            if (ui.stream >= 0) {
+                // own keys t are seen at most by rows whose token is >= t
+                if (ui.k0 > w_tok_hi) wave_has_rows = false;
+                whole = ui.nk == kUnit && w_str_lo == ui.stream && w_str_hi == ui.stream &&
+                        ui.k0 + kUnit - 1 <= w_tok_lo;
+            }
+        }
         const unsigned char* kbuf = lds + (st % C::NSTAGE) * C::STAGE;
         const unsigned char* vbuf = kbuf + C::STAGE_K;
         if (wave_has_rows) {
-            if (ui.stream < 0 && ui.nk == kUnit && (!PLAN || ui.k0 + kUnit <= vi.plan0)) {
+            if (whole) {
 #pragma unroll
                 for (int b = 0; b < C::KW / 32; ++b) block(std::false_type{}, kbuf, vbuf, kg * C::KW + 32 * b, ui);
             } else {

@@ -127,7 +127,12 @@ Plan make_plan(const pdec_dims* d, int num_videos)
     const long own_units_max = (long)ev * ceil_div(d->event_cap, kUnitKeys);
     const long units_max = ceil_div(d->max_prefix_len, kUnitKeys) + own_units_max;
     const long tokens = d->prefix_tokens > 0 ? d->prefix_tokens : (long)num_videos * d->max_prefix_len;
-    const long units_expected = ceil_div(tokens, kUnitKeys) + (long)d->num_events;
+    // a decode step's streams hold about one unit each; whole branches hold
+    // up to min(cap, Q) rows each (one stream with an empty prefix and the
+    // prefix as its rows is plain causal attention over it)
+    const long own_expected = qps > 1 ? (long)d->num_events * ceil_div(std::min<long>(d->event_cap, qps), kUnitKeys)
+                                      : (long)d->num_events;
+    const long units_expected = ceil_div(tokens, kUnitKeys) + own_expected;
     long upc = ceil_div(units_expected * d->num_kv_heads * p.rg_max, kTargetItems);
     if (path == kPathValu) {
         // four waves per item, each taking every fourth unit: a multiple of 4

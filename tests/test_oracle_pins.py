@@ -725,3 +725,24 @@ def test_causal_across_branches_sees_only_earlier_positions():
     f1, _ = oracle.attn_prefill(q[:1], kp, vp, ke[:1], ve[:1], n[:1], [0, kp.shape[0]], [0, 1], cross=1)
     f0, _ = oracle.attn_prefill(q[:1], kp, vp, ke[:1], ve[:1], n[:1], [0, kp.shape[0]], [0, 1])
     assert np.array_equal(f0, f1)
+
+
+def test_one_branch_over_an_empty_prefix_is_causal_attention():
+    """The prefix's own attention (§3.4: ordinary causal attention over the
+    shared prefix) is the whole-branch form with one stream, no shared
+    prefix and the prefix as that stream's rows: it equals softmax over the
+    lower-triangular scores, per head with its kv head h // G."""
+    from scipy.special import softmax
+    rng = np.random.default_rng(31)
+    Q, H_q, H_kv, D = 45, 6, 2, 16
+    q = rng.standard_normal((1, Q, H_q, D)).astype(np.float32)
+    ke = rng.standard_normal((1, Q, H_kv, D)).astype(np.float32)
+    ve = rng.standard_normal((1, Q, H_kv, D)).astype(np.float32)
+    empty = np.zeros((0, H_kv, D), np.float32)
+    out, lse = oracle.attn_prefill(q, empty, empty, ke, ve, [Q], [0, 0], [0, 1])
+    G = H_q // H_kv
+    for h in range(H_q):
+        s = (q[0, :, h, :].astype(np.float64) @ ke[0, :, h // G, :].T.astype(np.float64)) / np.sqrt(D)
+        s[np.triu_indices(Q, 1)] = -np.inf
+        np.testing.assert_allclose(out[0, :, h, :], softmax(s, axis=1) @ ve[0, :, h // G, :], atol=1e-12)
+        np.testing.assert_allclose(lse[0, :, h], np.log(np.exp(s).sum(axis=1)), atol=1e-12)

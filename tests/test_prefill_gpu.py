@@ -119,3 +119,45 @@ def test_causal_across_branches_sees_only_earlier_positions_bitwise():
     others = [0, 1, 3]
     assert torch.equal(out2[others, :7].view(torch.int16), out[others, :7].view(torch.int16))
     assert not torch.equal(out2[others, 7:], out[others, 7:])
+
+
+CAUSAL = [
+    # seed, Q (tokens), H_q, H_kv, D
+    (11, 300, 28, 4, 128),
+    (12, 1000, 8, 2, 64),
+    (13, 130, 28, 4, 128),
+    (14, 64, 4, 4, 64),
+    (15, 65, 7, 1, 128),
+]
+
+
+@pytest.mark.parametrize("case", CAUSAL, ids=[f"Q{c[1]}h{c[2]}x{c[3]}d{c[4]}" for c in CAUSAL])
+def test_prefix_causal_attention_matches_oracle(case):
+    """The prefix's own causal attention: one stream, no shared prefix, the
+    prefix as the stream's rows and one query per prefix token.  Exercises
+    the skip of units above a wave's tokens and the unmasked path for units
+    below them."""
+    seed, Q, H_q, H_kv, D = case
+    c = _case(seed, 1, Q, 0, [Q], H_q, H_kv, D)
+    out, lse = _run(c)
+    ref_o, ref_l = _ref(c)
+    check("bf16", host(out).reshape(Q, H_q, D), host(lse).reshape(Q, H_q), ref_o.reshape(Q, H_q, D),
+          ref_l.reshape(Q, H_q), what=f"causal prefix case {seed}")
+
+
+def test_prefix_causal_attention_32k_sampled_rows():
+    """Causal attention over a 32768-token prefix (the bench's workload), 29
+    sampled query tokens against the oracle's decode step holding j + 1 rows."""
+    Q, H_q, H_kv, D = 32768, 28, 4, 128
+    c = _case(21, 1, Q, 0, [Q], H_q, H_kv, D)
+    out, lse = _run(c)
+    js = np.unique(np.concatenate([[0, 1, 63, 64, 65, 4095, Q - 1],
+                                   np.random.default_rng(3).choice(Q, 22, replace=False)]))
+    got_o, got_l = host(out)[0, js], host(lse)[0, js]
+    ref_o = np.zeros((js.size, H_q, D))
+    ref_l = np.zeros((js.size, H_q))
+    for i, j in enumerate(js):
+        o, l = oracle.attn_step(c["q"][:, j], c["kp"], c["vp"], c["ke"], c["ve"], np.array([j + 1], np.int32),
+                                [0, 0], [0, 1])
+        ref_o[i], ref_l[i] = o[0], l[0]
+    check("bf16", got_o, got_l, ref_o, ref_l, what="causal prefix 32k")
