@@ -8,7 +8,7 @@
 // used by all of those rows; an own unit of stream f is used by f's rows
 // only.
 //
-// Work-group: 8 waves = WR row waves x WK key groups.  Row wave rw owns NT
+// Work-group: 8 or 16 waves = WR row waves x WK key groups.  Row wave rw owns NT
 // 16-row tiles; key group kg owns a contiguous 64/WK-key slice of every
 // 64-key stage (one unit).  Keys stream through a 4-stage LDS ring filled by
 // global_load_lds_dwordx4 (direct HBM -> LDS DMA, 1 KB per wave
@@ -101,7 +101,7 @@ struct MfmaCfg {
     static constexpr int DT = D / 16;
     static constexpr int RT = 16 * NT * WR;       // rows per item
     static constexpr int LDS = NSTAGE * STAGE;
-    static_assert(NW == 8, "eight waves");
+    static_assert(NW == 8 || NW == 16, "eight or sixteen waves");
     static_assert(KW % 32 == 0, "key group slice is whole 32-key blocks");
     static_assert(DMA_PER_STAGE % NW == 0, "DMA split");
     // cross-key-group merge buffer fits in the ring
@@ -115,7 +115,7 @@ template <int D>
 __device__ inline int v_off(int key, int ch) { return key * (2 * D) + 16 * (ch ^ ((2 * key) & 6)); }
 
 template <int D, int NT, int WR, int WK, bool PLAN, bool MQ>
-__global__ __launch_bounds__(512) void split_mfma_kernel(StepArgs a)
+__global__ __launch_bounds__(64 * WR * WK) void split_mfma_kernel(StepArgs a)
 {
     using C = MfmaCfg<D, NT, WR, WK>;
     __shared__ __attribute__((aligned(1024))) unsigned char lds[C::LDS];

@@ -109,9 +109,10 @@ Plan make_plan(const pdec_dims* d, int num_videos)
     if (qps > 1) path = kPathMfma;  // the vector kernels take one query per stream
     p.path = path;
     if (path == kPathMfma) {
-        // 8 waves: up to 4 tiles -> 1 tile per row wave, 2 key groups (64 rows);
-        // up to 8 -> 2 tiles per row wave, 2 key groups (128 rows);
-        // more -> 2 tiles per row wave, 8 row waves (256 rows per item)
+        // up to 4 tiles -> 8 waves: 1 tile per row wave, 2 key groups (64 rows);
+        // up to 8 -> 8 waves: 2 tiles per row wave, 2 key groups (128 rows);
+        // more -> 256 rows per item: 16 one-tile row waves (decode step,
+        // D = 128) or 8 two-tile row waves (whole branches, D = 64)
         const long tiles = ceil_div(rows_max, 16);
         p.shape = tiles <= 4 ? 1 : tiles <= 8 ? 2 : 3;
         p.rows_per_item = tiles <= 4 ? 64 : tiles <= 8 ? 128 : 256;

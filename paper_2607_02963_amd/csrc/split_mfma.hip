@@ -19,7 +19,17 @@ void launch_shape(const StepArgs& a, int shape, int grid, hipStream_t s)
     switch (shape) {
     case 1: hipLaunchKernelGGL((split_mfma_kernel<D, 1, 4, 2, PLAN, MQ>), dim3(grid), dim3(512), 0, s, a); break;
     case 2: hipLaunchKernelGGL((split_mfma_kernel<D, 2, 4, 2, PLAN, MQ>), dim3(grid), dim3(512), 0, s, a); break;
-    default: hipLaunchKernelGGL((split_mfma_kernel<D, 2, 8, 1, PLAN, MQ>), dim3(grid), dim3(512), 0, s, a); break;
+    default:
+        // 256 rows: sixteen one-tile row waves for the decode step at D = 128
+        // (four waves per SIMD hide more latency than eight two-tile waves);
+        // eight two-tile waves for whole branches, whose masked blocks run
+        // faster that way, and at D = 64, whose sixteen-wave form the
+        // compiler gives private-memory arrays
+        if constexpr (D == 128 && !MQ)
+            hipLaunchKernelGGL((split_mfma_kernel<D, 1, 16, 1, PLAN, MQ>), dim3(grid), dim3(1024), 0, s, a);
+        else
+            hipLaunchKernelGGL((split_mfma_kernel<D, 2, 8, 1, PLAN, MQ>), dim3(grid), dim3(512), 0, s, a);
+        break;
     }
 }
 
