@@ -15,7 +15,8 @@
 // instruction, no staging registers), three stages in flight while the
 // fourth is consumed.  Each key row (D bf16) is stored as D/8 16-byte chunks
 // permuted by an XOR of the key index, so the matrix-core operand reads below
-// hit distinct LDS banks.
+// hit distinct LDS banks (the transposing V read takes 8 keys per 32-lane
+// phase, so the V permutation differs over 8 consecutive keys).
 //
 // Per 32-key block, with v_mfma_f32_16x16x32_bf16 (D = A(16x32) B(32x16)):
 //   S^T  = K  Q^T    A = K rows from LDS (16 keys x 32 d), B = Q^T (registers)
@@ -100,6 +101,10 @@ struct MfmaCfg {
     static constexpr int KSTEPS = D / 32;
     static constexpr int DT = D / 16;
     static constexpr int RT = 16 * NT * WR;       // rows per item
+    // V rows: chunk pairs XOR-permuted by the key, over 8 keys at D = 128 so
+    // that the 8 keys one 32-lane phase of the transposing read touches fill
+    // all banks (over 4 keys at D = 64, whose rows are half a bank period)
+    static constexpr int VSW = D == 128 ? 14 : 6;
     static constexpr int LDS = NSTAGE * STAGE;
     static_assert(NW == 8 || NW == 16, "eight or sixteen waves");
     static_assert(KW % 32 == 0, "key group slice is whole 32-key blocks");
@@ -112,7 +117,7 @@ struct MfmaCfg {
 template <int D>
 __device__ inline int k_off(int key, int ch) { return key * (2 * D) + 16 * (ch ^ (key % (D / 8))); }
 template <int D>
-__device__ inline int v_off(int key, int ch) { return key * (2 * D) + 16 * (ch ^ ((2 * key) & 6)); }
+__device__ inline int v_off(int key, int ch) { return key * (2 * D) + 16 * (ch ^ ((2 * key) & (D == 128 ? 14 : 6))); }
 
 template <int D, int NT, int WR, int WK, bool PLAN, bool MQ>
 __global__ __launch_bounds__(64 * WR * WK) void split_mfma_kernel(StepArgs a)
@@ -247,7 +252,7 @@ __global__ __launch_bounds__(64 * WR * WK) void split_mfma_kernel(StepArgs a)
             const int pk = is_v ? piece - C::DMA_PER_STAGE / 2 : piece;
             const int key = pk * C::KPI + lane / C::CH;
             const int slot = lane % C::CH;
-            const int ch = is_v ? (slot ^ ((2 * key) & 6)) : (slot ^ (key % C::CH));
+            const int ch = is_v ? (slot ^ ((2 * key) & C::VSW)) : (slot ^ (key % C::CH));
             const int gkey = min(key, ui.nk - 1);
             const uint16_t* src = (is_v ? vb : kb) + (long)gkey * stride + 8 * ch;
             unsigned char* dst = sbase + (is_v ? C::STAGE_K : 0) + pk * 1024;
@@ -281,7 +286,7 @@ __global__ __launch_bounds__(64 * WR * WK) void split_mfma_kernel(StepArgs a)
     for (int dt = 0; dt < C::DT; ++dt) {
         const int key = 4 * lg + (l16 >> 2);
         const int ch = 2 * dt + ((l16 & 3) >> 1);
-        voff[dt] = key * C::ROWB + 16 * (ch ^ (2 * (key & 3))) + 8 * (l16 & 1);
+        voff[dt] = key * C::ROWB + 16 * (ch ^ ((2 * key) & C::VSW)) + 8 * (l16 & 1);
     }
 
     // One 32-key block of this wave: S^T, online softmax, O^T += V^T P^T.
