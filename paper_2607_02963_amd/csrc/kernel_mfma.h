@@ -498,6 +498,22 @@ __global__ __launch_bounds__(64 * WR * WK) void split_mfma_kernel(StepArgs a)
             // o / l in bf16: a convex combination of V rows, so in V's range
             const float inv = l_part[nt] > 0.f ? 1.f / l_part[nt] : 0.f;
             uint16_t* dst = static_cast<uint16_t*>(a.part_o) + slot * D;
+            if (a.max_chunks == 1) {
+                // A single chunk holds the whole row: the host launches no
+                // finish pass, and the row's result is written here with the
+                // finish's arithmetic for one slot (the same bf16 values and
+                // lse), an ended stream giving 0 and -inf.
+                const bool ended = a.event_lens[qr / ((long)a.H_q * a.qps)] <= 0;
+                dst = static_cast<uint16_t*>(a.out) + qr * D;
+#pragma unroll
+                for (int dt = 0; dt < C::DT; ++dt) {
+                    const f32x4_t v = o[nt][dt];
+                    const uint2 val = make_uint2(pack_bf16x2(v[0] * inv, v[1] * inv), pack_bf16x2(v[2] * inv, v[3] * inv));
+                    *reinterpret_cast<uint2*>(dst + 16 * dt + 4 * lg) = ended ? make_uint2(0u, 0u) : val;
+                }
+                if (a.lse && lg == 0) a.lse[qr] = ended ? kNegInf : kLn2 * (m_ref[nt] + __log2f(l_part[nt]));
+                continue;
+            }
 #pragma unroll
             for (int dt = 0; dt < C::DT; ++dt) {
                 const f32x4_t v = o[nt][dt];

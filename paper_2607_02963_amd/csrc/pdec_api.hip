@@ -255,6 +255,8 @@ int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_pr
     if ((rc = launch_status()) != PDEC_OK) return rc;
     if (timer_slot >= 0 && hipEventRecord(static_cast<hipEvent_t>(g_timer_stop[timer_slot]), s) != hipSuccess)
         return PDEC_ERR_HIP;
+    // one chunk per row on the matrix-core path: the split pass wrote the result
+    if (p.path == kPathMfma && p.max_chunks == 1) return PDEC_OK;
     const int fgrid = (int)rows;
     const dim3 fblock(256);
     if (bf16) {

@@ -161,3 +161,19 @@ def test_prefix_causal_attention_32k_sampled_rows():
                                 [0, 0], [0, 1])
         ref_o[i], ref_l[i] = o[0], l[0]
     check("bf16", got_o, got_l, ref_o, ref_l, what="causal prefix 32k")
+
+
+def test_single_chunk_launch_writes_results_and_ends_streams():
+    """40 branches of 64 tokens over an empty prefix plan to a single chunk
+    per row: the split pass then writes out and lse itself (no finish pass),
+    ended streams included (0 and -inf)."""
+    lens = [64] * 40
+    lens[3], lens[17] = 0, 0
+    lens[5], lens[30] = 1, 37
+    c = _case(41, 40, 64, 0, lens, 28, 4, 128, cap=64)
+    out, lse = _run(c)
+    ref_o, ref_l = _ref(c)
+    E, N = 40, 64
+    check("bf16", host(out).reshape(E * N, 28, 128), host(lse).reshape(E * N, 28), ref_o.reshape(E * N, 28, 128),
+          ref_l.reshape(E * N, 28), what="single-chunk whole branches")
+    assert torch.all(out[[3, 17]].float() == 0) and torch.all(torch.isneginf(lse[[3, 17]]))
