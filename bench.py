@@ -379,8 +379,10 @@ def run_prefill(args, torch, pdec, wl):
     dims = pdec.make_dims(E, H_q, H_kv, D, N, L, pdec.PDEC_DTYPE_BF16, queries_per_stream=N)
     ws = torch.empty(pdec.workspace_size(dims), dtype=torch.uint8, device="cuda")
 
+    cross = 1 if args.cross_causal else 0
+
     def call():
-        pdec.attn_prefill(q, kp, vp, ke, ve, lens, plen, out=out, lse=lse, workspace=ws)
+        pdec.attn_prefill(q, kp, vp, ke, ve, lens, plen, out=out, lse=lse, workspace=ws, cross=cross)
 
     for _ in range(args.warmup):
         call()
@@ -392,16 +394,19 @@ def run_prefill(args, torch, pdec, wl):
     e1.record()
     torch.cuda.synchronize()
     us = e0.elapsed_time(e1) / args.steps * 1e3
-    keys = E * H_q * sum(L + j + 1 for j in range(N))  # visible keys summed over query rows
+    # visible keys summed over query rows: the prefix and the branch up to j,
+    # and with Table 8's causal-attention row the other branches' rows < j
+    keys = E * H_q * sum(L + j + 1 + cross * (E - 1) * j for j in range(N))
     flops = 4 * D * keys
     tflops = flops / (us * 1e-6) / 1e12
     _log(f"bench: prefill {us:.1f} us/call, {flops / 1e9:.1f} GFLOP, {tflops:.1f} TFLOP/s")
     rec = {
-        "metric": "us per whole-branch attention call (13 branches x 48 tokens over a 32768-token prefix)",
+        "metric": "us per whole-branch attention call (13 branches x 48 tokens over a 32768-token prefix)"
+                  + (", causal attention across branches (Table 8)" if cross else ""),
         "value": round(us, 2), "unit": "us/call", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "higher_is_better": False, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": "prefill_L32768_E13_N48", "prefix_len": L, "branches": E, "tokens_per_branch": N,
-                   "H_q": H_q, "H_kv": H_kv, "head_dim": D},
+        "config": {"workload": "prefill_L32768_E13_N48" + ("_cross_causal" if cross else ""), "prefix_len": L,
+                   "branches": E, "tokens_per_branch": N, "H_q": H_q, "H_kv": H_kv, "head_dim": D},
         "roofline": {"bound": "mfma", "achieved": round(tflops, 1), "peak": 2500.0, "unit": "TFLOP/s",
                      "frac": round(tflops / 2500.0, 4), "traffic": None, "kernel": "split pass + finish (per call)",
                      "kernel_us": round(us, 2), "kernel_algorithmic_flops": flops},
@@ -471,6 +476,9 @@ def main():
     ap.add_argument("--plan-mask", choices=("full", "self"), default="full",
                     help="full: every stream sees all plan tokens (the full design); self: each stream sees only "
                          "its own run of the workload's plan tokens (Table 8 'self G-token only')")
+    ap.add_argument("--cross-causal", action="store_true",
+                    help="prefill workload: Table 8's 'causal attention' row, each query also seeing the other "
+                         "branches' rows at earlier positions")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MB (5 times) and exit; "
                          "used to calibrate the HBM byte counters")
