@@ -264,6 +264,44 @@ def attn_prefill(q, k_prefix, v_prefix, k_event, v_event, event_lens, prefix_len
     return out, lse
 
 
+def attn_prefill_ragged(q, k_prefix, v_prefix, cu_prefix, k_event, v_event, event_lens, cu_events, *,
+                        max_prefix_len, max_events_per_video, out=None, lse=None, workspace=None, scale=0.0,
+                        stream=None, cross=0):
+    """Whole branches over a ragged batch of videos (``pdec_attn_step_ragged``
+    with ``queries_per_stream`` N); returns (out [SE,N,H_q,D], lse [SE,N,H_q]).
+
+    q [SE,N,H_q,D] bf16; the rest as for ``attn_step_ragged``; visibility as
+    for ``attn_prefill``, within each video.
+    """
+    SE, N, H_q, D = q.shape
+    H_kv = k_prefix.shape[1]
+    cap = k_event.shape[1]
+    V = cu_prefix.shape[0] - 1
+    dims = make_dims(SE, H_q, H_kv, D, cap, max_prefix_len, _dtype_code(q), scale, max_events_per_video,
+                     prefix_tokens=k_prefix.shape[0], queries_per_stream=N, cross_causal=cross)
+    ws_bytes = workspace_size(dims, V)
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None:
+        lse = torch.empty((SE, N, H_q), dtype=torch.float32, device=q.device)
+    if workspace is None:
+        workspace = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device=q.device)
+    if cu_events.shape[0] != V + 1 or k_event.shape[0] != SE or event_lens.shape[0] != SE:
+        raise ValueError("inconsistent batch shapes")
+    if v_prefix.shape != k_prefix.shape or v_event.shape != k_event.shape or out.shape != q.shape \
+            or lse.shape != (SE, N, H_q):
+        raise ValueError("inconsistent K/V / out / lse shapes")
+    args = [ctypes.c_int32(V), _dev(q, "q", ndim=4), _dev(k_prefix, "k_prefix", q.dtype, 3),
+            _dev(v_prefix, "v_prefix", q.dtype, 3), _dev(cu_prefix, "cu_prefix", torch.int32, 1),
+            _dev(k_event, "k_event", q.dtype, 4), _dev(v_event, "v_event", q.dtype, 4),
+            _dev(event_lens, "event_lens", torch.int32, 1), _dev(cu_events, "cu_events", torch.int32, 1),
+            _dev(out, "out", q.dtype, 4), _dev(lse, "lse", torch.float32, 3),
+            _dev(workspace, "workspace"), ctypes.c_size_t(workspace.numel() * workspace.element_size()),
+            _stream(stream, q.device)]
+    _check("pdec_attn_step_ragged", lib().pdec_attn_step_ragged(ctypes.byref(dims), *args))
+    return out, lse
+
+
 def attn_step_ragged(q, k_prefix, v_prefix, cu_prefix, k_event, v_event, event_lens, cu_events, *,
                      max_prefix_len, max_events_per_video, out=None, lse=None, workspace=None, scale=0.0,
                      stream=None, want_lse=True, plan_mask=0, plan_per_stream=0):

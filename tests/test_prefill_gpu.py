@@ -177,3 +177,27 @@ def test_single_chunk_launch_writes_results_and_ends_streams():
     check("bf16", host(out).reshape(E * N, 28, 128), host(lse).reshape(E * N, 28), ref_o.reshape(E * N, 28, 128),
           ref_l.reshape(E * N, 28), what="single-chunk whole branches")
     assert torch.all(out[[3, 17]].float() == 0) and torch.all(torch.isneginf(lse[[3, 17]]))
+
+
+@pytest.mark.parametrize("cross", [0, 1])
+def test_prefill_ragged_videos_matches_oracle(cross):
+    """Whole branches over three videos of their own prefix lengths and
+    stream counts (one video without a prefix), through the ragged entry."""
+    rng = np.random.default_rng(61 + cross)
+    H_q, H_kv, D, N, cap = 28, 4, 128, 20, 20
+    Ls, Es = [700, 0, 1300], [3, 2, 5]
+    f = lambda *shape: wl.bf16_bits((0.5 * rng.standard_normal(shape)).astype(np.float32))  # noqa: E731
+    SE, SL = sum(Es), sum(Ls)
+    q, kp, vp = f(SE, N, H_q, D), f(SL, H_kv, D), f(SL, H_kv, D)
+    ke, ve = f(SE, cap, H_kv, D), f(SE, cap, H_kv, D)
+    n = np.array([20, 7, 0, 20, 1, 20, 20, 13, 20, 5], np.int32)
+    cu_p = np.concatenate([[0], np.cumsum(Ls)]).astype(np.int32)
+    cu_e = np.concatenate([[0], np.cumsum(Es)]).astype(np.int32)
+    out, lse = pdec.attn_prefill_ragged(dev_float(q, "bf16"), dev_float(kp, "bf16"), dev_float(vp, "bf16"),
+                                        dev_int(cu_p), dev_float(ke, "bf16"), dev_float(ve, "bf16"), dev_int(n),
+                                        dev_int(cu_e), max_prefix_len=max(Ls), max_events_per_video=max(Es),
+                                        cross=cross)
+    torch.cuda.synchronize()
+    ref_o, ref_l = oracle.attn_prefill(q, kp, vp, ke, ve, n, cu_p, cu_e, cross=cross)
+    check("bf16", host(out).reshape(SE * N, H_q, D), host(lse).reshape(SE * N, H_q), ref_o.reshape(SE * N, H_q, D),
+          ref_l.reshape(SE * N, H_q), what=f"ragged prefill cross={cross}")
