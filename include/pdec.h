@@ -315,6 +315,45 @@ int pdec_aggregate(const pdec_aggr_dims* dims, const void* g, const void* x, con
                    const uint8_t* salient, const float* scores, const void* q, const void* k, const float* lse,
                    float* weights, void* out, void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * Backward pass of the whole-branch attention (the training form of the §3.4
+ * mask, as computed by pdec_attn_step with queries_per_stream N >= 1), for
+ * one video.  Given the forward's out and lse and the gradient dout of a loss
+ * with respect to out, for every live query row i (stream e with n_e > 0,
+ * token j, head h) and every key k it sees (the prefix and its own rows
+ * 0 .. min(j, n_e - 1)):
+ *   p_ik = exp(scale <q_i, k_k> - lse_i),   D_i = <dout_i, out_i>,
+ *   ds_ik = p_ik (<dout_i, v_k> - D_i),
+ *   dq_i = scale sum_k ds_ik k_k,  dk_k = scale sum_i ds_ik q_i,  dv_k = sum_i p_ik dout_i.
+ * Rows of ended streams add nothing; keys no row sees get 0.  With one stream
+ * and no prefix (the prefix as the stream's rows) this is the backward of
+ * plain causal attention.  dims as for pdec_attn_step: bf16, head_dim 64 or
+ * 128, plan_mask 0 and cross_causal 0 (else PDEC_ERR_UNSUPPORTED).
+ * P and ds meet the matrix cores in bf16, as the forward's P does; every
+ * sum is float32.
+ */
+/* Workspace bytes for pdec_attn_prefill_backward (0 for invalid dims). Host only. */
+size_t pdec_backward_workspace_size(const pdec_dims* dims);
+
+/*
+ *   q, out, dout [E, N, H_q, D]   device, bf16, 16-byte aligned;
+ *   k_prefix, v_prefix [Lmax, H_kv, D], k_event, v_event [E, cap, H_kv, D]
+ *                                 device, bf16, as for the forward call;
+ *   event_lens [E], prefix_lens [1] device int32, as for the forward call;
+ *   lse [E, N, H_q]               device, float32, the forward's lse;
+ *   dq [E, N, H_q, D], dk_prefix, dv_prefix [Lmax, H_kv, D],
+ *   dk_event, dv_event [E, cap, H_kv, D]
+ *                                 device, float32, 16-byte aligned, every element written;
+ *   workspace >= pdec_backward_workspace_size(dims) bytes, device.
+ * Prefix pointers may be NULL when max_prefix_len is 0.  Asynchronous on
+ * `stream` (three launches).  Returns a pdec_status.
+ */
+int pdec_attn_prefill_backward(const pdec_dims* dims, const void* q, const void* k_prefix, const void* v_prefix,
+                               const void* k_event, const void* v_event, const int32_t* event_lens,
+                               const int32_t* prefix_lens, const void* out, const float* lse, const void* dout,
+                               float* dq, float* dk_prefix, float* dv_prefix, float* dk_event, float* dv_event,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -28,7 +28,8 @@ PATH_AUTO, PATH_VALU, PATH_MFMA = 0, 1, 2
 EXPORTED = ("pdec_strerror", "pdec_workspace_size", "pdec_attn_step", "pdec_attn_step_ragged",
             "pdec_kv_append", "pdec_rope_kv_append", "pdec_set_path", "pdec_query_plan",
             "pdec_set_split_timer", "pdec_grounding_workspace_size", "pdec_segment_grounding",
-            "pdec_aggregation_workspace_size", "pdec_aggregate")
+            "pdec_aggregation_workspace_size", "pdec_aggregate", "pdec_backward_workspace_size",
+            "pdec_attn_prefill_backward")
 
 AGGR_MODES = {"uniform": 0, "learned": 1, "attention": 2}
 
@@ -106,6 +107,10 @@ def lib():
         L.pdec_aggregation_workspace_size.argtypes = [ap]
         L.pdec_aggregate.restype = ctypes.c_int
         L.pdec_aggregate.argtypes = [ap, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.pdec_backward_workspace_size.restype = ctypes.c_size_t
+        L.pdec_backward_workspace_size.argtypes = [dp]
+        L.pdec_attn_prefill_backward.restype = ctypes.c_int
+        L.pdec_attn_prefill_backward.argtypes = [dp] + [vp] * 16 + [sz, vp]
         L.pdec_set_path.restype = ctypes.c_int
         L.pdec_set_path.argtypes = [ctypes.c_int]
         L.pdec_query_plan.restype = ctypes.c_int
@@ -262,6 +267,40 @@ def attn_prefill(q, k_prefix, v_prefix, k_event, v_event, event_lens, prefix_len
             _stream(stream, q.device)]
     _check("pdec_attn_step", lib().pdec_attn_step(ctypes.byref(dims), *args))
     return out, lse
+
+
+def attn_prefill_backward(q, k_prefix, v_prefix, k_event, v_event, event_lens, prefix_lens, out, lse, dout, *,
+                          max_prefix_len=None, scale=0.0, workspace=None, stream=None):
+    """Gradients of ``attn_prefill`` (``pdec_attn_prefill_backward``) given the
+    forward's out and lse and dout; returns float32 (dq, dk_prefix, dv_prefix,
+    dk_event, dv_event) shaped like q, k_prefix and k_event.
+    """
+    E, N, H_q, D = q.shape
+    H_kv = k_prefix.shape[1]
+    cap = k_event.shape[1]
+    if max_prefix_len is None:
+        max_prefix_len = k_prefix.shape[0]
+    dims = make_dims(E, H_q, H_kv, D, cap, max_prefix_len, _dtype_code(q), scale, queries_per_stream=N)
+    ws_bytes = int(lib().pdec_backward_workspace_size(ctypes.byref(dims)))
+    if workspace is None:
+        workspace = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device=q.device)
+    if out.shape != q.shape or dout.shape != q.shape or lse.shape != (E, N, H_q):
+        raise ValueError("out / dout / lse shapes")
+    if v_prefix.shape != k_prefix.shape or v_event.shape != k_event.shape or k_event.shape[0] != E:
+        raise ValueError("inconsistent K/V shapes")
+    f32 = dict(dtype=torch.float32, device=q.device)
+    dq = torch.empty(q.shape, **f32)
+    dkp, dvp = torch.empty(k_prefix.shape, **f32), torch.empty(k_prefix.shape, **f32)
+    dke, dve = torch.empty(k_event.shape, **f32), torch.empty(k_event.shape, **f32)
+    args = [_dev(q, "q", ndim=4), _dev(k_prefix, "k_prefix", q.dtype, 3), _dev(v_prefix, "v_prefix", q.dtype, 3),
+            _dev(k_event, "k_event", q.dtype, 4), _dev(v_event, "v_event", q.dtype, 4),
+            _dev(event_lens, "event_lens", torch.int32, 1), _dev(prefix_lens, "prefix_lens", torch.int32, 1),
+            _dev(out, "out", q.dtype, 4), _dev(lse, "lse", torch.float32, 3), _dev(dout, "dout", q.dtype, 4),
+            _dev(dq, "dq"), _dev(dkp, "dk_prefix"), _dev(dvp, "dv_prefix"), _dev(dke, "dk_event"),
+            _dev(dve, "dv_event"), _dev(workspace, "workspace"),
+            ctypes.c_size_t(workspace.numel() * workspace.element_size()), _stream(stream, q.device)]
+    _check("pdec_attn_prefill_backward", lib().pdec_attn_prefill_backward(ctypes.byref(dims), *args))
+    return dq, dkp, dvp, dke, dve
 
 
 def attn_prefill_ragged(q, k_prefix, v_prefix, cu_prefix, k_event, v_event, event_lens, cu_events, *,

@@ -173,3 +173,24 @@ def test_aggregate_rejects_bad_arguments_before_any_launch():
     # workspace too small
     assert L.pdec_aggregate(ctypes.byref(d), p, p, p, p, p, None, None, None, None, p, ws,
                             ctypes.c_size_t(16), None) == pdec.PDEC_ERR_WORKSPACE
+
+
+def test_backward_dims_checks():
+    ok = pdec.make_dims(13, 28, 4, 128, 48, 32768, pdec.PDEC_DTYPE_BF16, queries_per_stream=48)
+    assert pdec.lib().pdec_backward_workspace_size(ctypes.byref(ok)) == 13 * 48 * 28 * 4
+    bad = [pdec.make_dims(13, 28, 4, 128, 48, 32768, pdec.PDEC_DTYPE_F32, queries_per_stream=48),
+           pdec.make_dims(13, 28, 4, 96, 48, 32768, pdec.PDEC_DTYPE_BF16, queries_per_stream=48),
+           pdec.make_dims(13, 28, 5, 128, 48, 32768, pdec.PDEC_DTYPE_BF16, queries_per_stream=48),
+           pdec.make_dims(13, 28, 4, 128, 48, 32768, pdec.PDEC_DTYPE_BF16, queries_per_stream=48, cross_causal=1),
+           pdec.make_dims(13, 28, 4, 128, 48, 32768, pdec.PDEC_DTYPE_BF16, plan_mask=1, plan_per_stream=2)]
+    for d in bad:
+        assert pdec.lib().pdec_backward_workspace_size(ctypes.byref(d)) == 0
+    p = ctypes.c_void_p(4096)
+    ws = ctypes.c_void_p(256)
+    # misaligned dq, then a short workspace: refused before any launch
+    args = [p] * 10 + [ctypes.c_void_p(4100)] + [p] * 4
+    assert pdec.lib().pdec_attn_prefill_backward(ctypes.byref(ok), *args, ws, ctypes.c_size_t(1 << 30), None) \
+        == pdec.PDEC_ERR_INVALID_ARG
+    args = [p] * 15
+    assert pdec.lib().pdec_attn_prefill_backward(ctypes.byref(ok), *args, ws, ctypes.c_size_t(16), None) \
+        == pdec.PDEC_ERR_WORKSPACE

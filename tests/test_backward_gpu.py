@@ -1,0 +1,88 @@
+"""Backward pass of the whole-branch attention on the GPU
+(pdec_attn_prefill_backward) against the oracle (oracle/backward.py).
+
+Both take the same inputs: the GPU forward's out (bf16) and lse, and a
+seeded dout.  The kernel meets the matrix cores with P and ds rounded to
+bf16, as the forward does with P; the bar is the bf16 one of the forward,
+taken relative to each gradient's scale: normwise relative error <= 1e-2 and
+max-abs error <= 2e-2 x max |gradient|.  Cache rows no query sees must be
+exactly 0, and an ended stream's dq exactly 0.
+"""
+import numpy as np
+import pytest
+import torch
+
+import backward
+from gpu_util import dev_float, dev_int
+from paper_2607_02963_amd import pdec
+from paper_2607_02963_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+
+def _case(seed, E, N, L, lens, H_q, H_kv, D, cap=None, sigma=0.5):
+    rng = np.random.default_rng(seed)
+    cap = cap or N
+    f = lambda *shape: wl.bf16_bits((sigma * rng.standard_normal(shape)).astype(np.float32))  # noqa: E731
+    return dict(q=f(E, N, H_q, D), kp=f(L, H_kv, D), vp=f(L, H_kv, D), ke=f(E, cap, H_kv, D),
+                ve=f(E, cap, H_kv, D), do=f(E, N, H_q, D), n=np.asarray(lens, np.int32), L=L)
+
+
+def _close(got, ref, what):
+    got, ref = got.astype(np.float64), ref.astype(np.float64)
+    scale = max(float(np.abs(ref).max()), 1e-30)
+    norm = np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-30)
+    assert norm <= 1e-2, (what, "normwise", norm)
+    assert float(np.abs(got - ref).max()) <= 2e-2 * scale, (what, "max-abs", float(np.abs(got - ref).max()), scale)
+
+
+def _run_and_check(c):
+    d = {k: dev_float(c[k], "bf16") for k in ("q", "kp", "vp", "ke", "ve", "do")}
+    n, plen = dev_int(c["n"]), dev_int([c["L"]])
+    out, lse = pdec.attn_prefill(d["q"], d["kp"], d["vp"], d["ke"], d["ve"], n, plen)
+    grads = pdec.attn_prefill_backward(d["q"], d["kp"], d["vp"], d["ke"], d["ve"], n, plen, out, lse, d["do"])
+    torch.cuda.synchronize()
+    got = [g.cpu().numpy() for g in grads]
+    out_h = out.cpu().view(torch.int16).numpy().view(np.uint16)
+    ref = backward.attn_prefill_backward(c["q"], c["kp"], c["vp"], c["ke"], c["ve"], c["n"], out_h,
+                                         lse.cpu().numpy(), c["do"])
+    for name, g, r in zip(("dq", "dk_prefix", "dv_prefix", "dk_event", "dv_event"), got, ref):
+        if r.size:
+            _close(g, r, name)
+    for e, ne in enumerate(c["n"]):
+        assert np.all(got[3][e, max(ne, 0):] == 0) and np.all(got[4][e, max(ne, 0):] == 0)
+        if ne <= 0:
+            assert np.all(got[0][e] == 0)
+    return got
+
+
+CASES = [
+    # seed, E, N, L, lens, H_q, H_kv, D
+    (1, 3, 5, 700, [5, 3, 0], 28, 4, 128),
+    (2, 4, 16, 1000, [16, 16, 9, 1], 28, 4, 128),
+    (3, 6, 7, 515, [7, 7, 7, 7, 7, 7], 16, 2, 64),
+    (4, 1, 70, 300, [70], 8, 1, 128),
+    (5, 2, 3, 64, [3, 2], 4, 4, 64),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[f"E{c[1]}N{c[2]}L{c[3]}d{c[7]}" for c in CASES])
+def test_backward_matches_oracle(case):
+    seed, E, N, L, lens, H_q, H_kv, D = case
+    _run_and_check(_case(seed, E, N, L, lens, H_q, H_kv, D))
+
+
+def test_backward_of_causal_attention_over_the_prefix():
+    """One stream, no shared prefix, the prefix as its rows: the backward of
+    plain causal attention, 200 tokens spanning four 64-key units."""
+    _run_and_check(_case(6, 1, 200, 0, [200], 28, 4, 128))
+
+
+def test_backward_cache_longer_than_branch_and_repeatable():
+    """Caches with room past the branch (rows nobody sees stay 0), and two
+    calls agree bit for bit."""
+    c = _case(7, 3, 9, 130, [9, 4, 6], 8, 2, 128, cap=70)
+    a = _run_and_check(c)
+    b = _run_and_check(c)
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
