@@ -414,6 +414,60 @@ def run_prefill(args, torch, pdec, wl):
     print(json.dumps(rec), flush=True)
 
 
+def run_prefill_backward(args, torch, pdec, wl):
+    """Backward pass of the prefill workload (13 branches x 48 tokens over a
+    32768-token prefix, H_q 28, H_kv 4, D 128, bf16): dq, dk and dv of the
+    prefix and of the branches, from the forward's out and lse and a seeded
+    dout.  Algorithmic flops: the five products of the backward (S, dP, dV,
+    dK, dQ), 10 * D per visible (row, key) pair; the kernels' recomputation
+    of S and dP for dQ is not counted.  µs per call from HIP events around K
+    back-to-back calls."""
+    E, N, L, H_q, H_kv, D = 13, 48, 32768, 28, 4, 128
+    rng = np.random.default_rng(8)
+
+    def f(*shape):
+        a = wl.bf16_bits((0.5 * rng.standard_normal(shape, dtype=np.float32)).astype(np.float32))
+        return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
+
+    q, kp, vp, ke, ve, do = f(E, N, H_q, D), f(L, H_kv, D), f(L, H_kv, D), f(E, N, H_kv, D), f(E, N, H_kv, D), \
+        f(E, N, H_q, D)
+    lens = torch.full((E,), N, dtype=torch.int32, device="cuda")
+    plen = torch.tensor([L], dtype=torch.int32, device="cuda")
+    out, lse = pdec.attn_prefill(q, kp, vp, ke, ve, lens, plen)
+    dims = pdec.make_dims(E, H_q, H_kv, D, N, L, pdec.PDEC_DTYPE_BF16, queries_per_stream=N)
+    ws = torch.empty(max(pdec.backward_workspace_size(dims), 16), dtype=torch.uint8, device="cuda")
+
+    def call():
+        pdec.attn_prefill_backward(q, kp, vp, ke, ve, lens, plen, out, lse, do, workspace=ws)
+
+    for _ in range(args.warmup):
+        call()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        call()
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) / args.steps * 1e3
+    keys = E * H_q * sum(L + j + 1 for j in range(N))  # visible keys summed over query rows
+    flops = 10 * D * keys
+    tflops = flops / (us * 1e-6) / 1e12
+    _log(f"bench: prefill backward {us:.1f} us/call, {flops / 1e9:.1f} GFLOP, {tflops:.1f} TFLOP/s")
+    rec = {
+        "metric": "us per whole-branch attention backward call (13 branches x 48 tokens over a 32768-token prefix)",
+        "value": round(us, 1), "unit": "us/call", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "higher_is_better": False, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "prefill_backward_L32768_E13_N48", "prefix_len": L, "branches": E,
+                   "tokens_per_branch": N, "H_q": H_q, "H_kv": H_kv, "head_dim": D},
+        "roofline": {"bound": "mfma", "achieved": round(tflops, 1), "peak": 2500.0, "unit": "TFLOP/s",
+                     "frac": round(tflops / 2500.0, 4), "traffic": None,
+                     "kernel": "bwd_drow + bwd_dkdv + bwd_dq (per call)", "kernel_us": round(us, 1),
+                     "kernel_algorithmic_flops": flops},
+    }
+    print(json.dumps(rec), flush=True)
+
+
 def run_prefix_causal(args, torch, pdec, wl):
     """The prefix's own causal attention over 32768 tokens (H_q 28, H_kv 4,
     D 128, bf16), run as whole branches: one stream, no shared prefix, the
@@ -471,7 +525,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="long_32k",
                     help="long_32k | single_8k | ragged_16 | tiny_f32 | loop_64 | rope_append | grounding | prefill"
-                         " | aggregation | prefix_causal")
+                         " | aggregation | prefix_causal | prefill_backward")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--plan-mask", choices=("full", "self"), default="full",
                     help="full: every stream sees all plan tokens (the full design); self: each stream sees only "
@@ -513,6 +567,9 @@ def main():
         return
     if args.workload == "grounding":
         run_grounding(args, torch, pdec, wl)
+        return
+    if args.workload == "prefill_backward":
+        run_prefill_backward(args, torch, pdec, wl)
         return
     if args.workload == "prefix_causal":
         run_prefix_causal(args, torch, pdec, wl)

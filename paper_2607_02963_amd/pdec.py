@@ -269,6 +269,10 @@ def attn_prefill(q, k_prefix, v_prefix, k_event, v_event, event_lens, prefix_len
     return out, lse
 
 
+def backward_workspace_size(dims: Dims) -> int:
+    return int(lib().pdec_backward_workspace_size(ctypes.byref(dims)))
+
+
 def attn_prefill_backward(q, k_prefix, v_prefix, k_event, v_event, event_lens, prefix_lens, out, lse, dout, *,
                           max_prefix_len=None, scale=0.0, workspace=None, stream=None):
     """Gradients of ``attn_prefill`` (``pdec_attn_prefill_backward``) given the
