@@ -15,8 +15,9 @@
 //  1. D_i for every row (16 lanes per row);
 //  2. dk, dv: one work-group per 64-key unit (a prefix unit, or 64 rows of
 //     one stream's cache) and kv head; wave w holds keys 16w .. 16w + 15 as
-//     the B operands of S = Q K^T and dP = dO V^T, and loops over the 16-row
-//     tiles of the rows that can see the unit, staged through LDS.  The S
+//     the B operands of S = Q K^T and dP = dO V^T, and loops over 64-row
+//     tiles of the rows that can see the unit, staged through LDS (four
+//     16-row sub-tiles between barriers).  The S
 //     accumulator gives a lane key l % 16 for rows 4(l/16) .. +3, which is the
 //     A operand (keys x rows) of dV += P^T dO and dK += dS^T Q; their B
 //     operands (rows x d) come from the row tiles with the transposing LDS
@@ -125,10 +126,12 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(BwdArgs a)
     constexpr int KS = D / 32;  // 32-wide d steps
     constexpr int DT = D / 16;  // 16-wide d blocks
     constexpr int CH = D / 8;   // 16-byte chunks per row
-    __shared__ __attribute__((aligned(16))) unsigned char qs[16 * 2 * D];
-    __shared__ __attribute__((aligned(16))) unsigned char dos[16 * 2 * D];
-    __shared__ float lse2_s[16], drow_s[16];
-    __shared__ int tok_s[16];
+    constexpr int TR = 64;      // rows per staged tile: four 16-row sub-tiles between barriers
+    constexpr int SPT = TR * CH / 256;  // staged chunks per thread (q and dO each)
+    __shared__ __attribute__((aligned(16))) unsigned char qs[TR * 2 * D];
+    __shared__ __attribute__((aligned(16))) unsigned char dos[TR * 2 * D];
+    __shared__ float lse2_s[TR], drow_s[TR];
+    __shared__ int tok_s[TR];
 
     const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, l16 = lane & 15, lg = lane >> 4;
     const int g = blockIdx.y;
@@ -178,21 +181,24 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(BwdArgs a)
         dv[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     }
 
-    // row-tile staging: thread tid moves chunk tid % CH of tile row tid / CH
-    const int srow = tid / CH, sch = tid % CH;
-    const bool stager = tid < 16 * CH;
-    auto fetch = [&](int rb, u32x4_t& qv, u32x4_t& dv4, float& l2, float& dr, int& tk) {
-        const int r = rb + srow;
-        qv = dv4 = u32x4_t{0u, 0u, 0u, 0u};
-        if (stager && r < r_end) {
-            const long qr = bwd_qrow(a, g, r);
-            qv = *reinterpret_cast<const u32x4_t*>(a.q + qr * D + 8 * sch);
-            dv4 = *reinterpret_cast<const u32x4_t*>(a.dout + qr * D + 8 * sch);
+    // row tiles of TR rows, staged through LDS; thread tid moves chunks
+    // tid + 256 m of the tile's TR x CH (q and dO) and, for tid < TR, the
+    // row's lse, D and token
+    auto fetch = [&](int rb, u32x4_t (&qv)[SPT], u32x4_t (&dv4)[SPT], float& l2, float& dr, int& tk) {
+#pragma unroll
+        for (int m = 0; m < SPT; ++m) {
+            const int cidx = tid + 256 * m, sr = cidx / CH, sc = cidx % CH, r = rb + sr;
+            qv[m] = dv4[m] = u32x4_t{0u, 0u, 0u, 0u};
+            if (r < r_end) {
+                const long qr = bwd_qrow(a, g, r);
+                qv[m] = *reinterpret_cast<const u32x4_t*>(a.q + qr * D + 8 * sc);
+                dv4[m] = *reinterpret_cast<const u32x4_t*>(a.dout + qr * D + 8 * sc);
+            }
         }
         l2 = __builtin_inff();  // p = 0 for rows past the range or of ended streams
         dr = 0.f;
         tk = 0;
-        if (tid < 16) {
+        if (tid < TR) {
             const int rr = rb + tid;
             if (rr < r_end) {
                 const int e = rr / (a.N * a.G);
@@ -206,48 +212,54 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(BwdArgs a)
         }
     };
 
-    u32x4_t qv, dv4;
+    u32x4_t qv[SPT], dv4[SPT];
     float l2, dr;
     int tk;
     if (r_begin < r_end) fetch(r_begin, qv, dv4, l2, dr, tk);
-    for (int rb = r_begin; rb < r_end; rb += 16) {
+    for (int rb = r_begin; rb < r_end; rb += TR) {
         __syncthreads();  // the previous tile is no longer read
-        if (stager) {
-            *reinterpret_cast<u32x4_t*>(qs + tile_off<D>(srow, sch)) = qv;
-            *reinterpret_cast<u32x4_t*>(dos + tile_off<D>(srow, sch)) = dv4;
+#pragma unroll
+        for (int m = 0; m < SPT; ++m) {
+            const int cidx = tid + 256 * m, sr = cidx / CH, sc = cidx % CH;
+            *reinterpret_cast<u32x4_t*>(qs + tile_off<D>(sr, sc)) = qv[m];
+            *reinterpret_cast<u32x4_t*>(dos + tile_off<D>(sr, sc)) = dv4[m];
         }
-        if (tid < 16) {
+        if (tid < TR) {
             lse2_s[tid] = l2;
             drow_s[tid] = dr;
             tok_s[tid] = tk;
         }
         __syncthreads();
-        if (rb + 16 < r_end) fetch(rb + 16, qv, dv4, l2, dr, tk);  // next tile, in flight meanwhile
+        if (rb + TR < r_end) fetch(rb + TR, qv, dv4, l2, dr, tk);  // next tile, in flight meanwhile
+        const int nsub = min(TR, r_end - rb + 15) / 16;  // 16-row sub-tiles holding rows of the range
 
-        // S = Q K^T and dP = dO V^T: lane holds rows 4 lg + i of key l16
-        f32x4_t s = {0.f, 0.f, 0.f, 0.f}, dp = {0.f, 0.f, 0.f, 0.f};
+        for (int sub = 0; sub < nsub; ++sub) {
+            const int r0 = 16 * sub;
+            // S = Q K^T and dP = dO V^T: lane holds rows r0 + 4 lg + i of key l16
+            f32x4_t sc4 = {0.f, 0.f, 0.f, 0.f}, dp = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int t = 0; t < KS; ++t) {
-            const u32x4_t qa = *reinterpret_cast<const u32x4_t*>(qs + tile_off<D>(l16, 4 * t + lg));
-            const u32x4_t da = *reinterpret_cast<const u32x4_t*>(dos + tile_off<D>(l16, 4 * t + lg));
-            s = mfma_16x16x32(as_bf16x8(qa), as_bf16x8(kB[t]), s);
-            dp = mfma_16x16x32(as_bf16x8(da), as_bf16x8(vB[t]), dp);
-        }
-        float p[4], ds[4];
+            for (int t = 0; t < KS; ++t) {
+                const u32x4_t qa = *reinterpret_cast<const u32x4_t*>(qs + tile_off<D>(r0 + l16, 4 * t + lg));
+                const u32x4_t da = *reinterpret_cast<const u32x4_t*>(dos + tile_off<D>(r0 + l16, 4 * t + lg));
+                sc4 = mfma_16x16x32(as_bf16x8(qa), as_bf16x8(kB[t]), sc4);
+                dp = mfma_16x16x32(as_bf16x8(da), as_bf16x8(vB[t]), dp);
+            }
+            float p[4], ds[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int rr = 4 * lg + i;
-            bool vis = kvalid;
-            if (own >= 0) vis = vis & (key <= tok_s[rr]);  // own row t seen by tokens j >= t
-            p[i] = vis ? fast_exp2(fmaf(s[i], a.c, -lse2_s[rr])) : 0.f;
-            ds[i] = p[i] * (dp[i] - drow_s[rr]);
-        }
-        const s16x4_t pa = pack_bf16x4(p[0], p[1], p[2], p[3]);
-        const s16x4_t dsa = pack_bf16x4(ds[0], ds[1], ds[2], ds[3]);
+            for (int i = 0; i < 4; ++i) {
+                const int rr = r0 + 4 * lg + i;
+                bool vis = kvalid;
+                if (own >= 0) vis = vis & (key <= tok_s[rr]);  // own row t seen by tokens j >= t
+                p[i] = vis ? fast_exp2(fmaf(sc4[i], a.c, -lse2_s[rr])) : 0.f;
+                ds[i] = p[i] * (dp[i] - drow_s[rr]);
+            }
+            const s16x4_t pa = pack_bf16x4(p[0], p[1], p[2], p[3]);
+            const s16x4_t dsa = pack_bf16x4(ds[0], ds[1], ds[2], ds[3]);
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-            dv[dt] = mfma_16x16x16(pa, tile_tr<D>(dos, 0, dt, l16, lg), dv[dt]);
-            dk[dt] = mfma_16x16x16(dsa, tile_tr<D>(qs, 0, dt, l16, lg), dk[dt]);
+            for (int dt = 0; dt < DT; ++dt) {
+                dv[dt] = mfma_16x16x16(pa, tile_tr<D>(dos, r0, dt, l16, lg), dv[dt]);
+                dk[dt] = mfma_16x16x16(dsa, tile_tr<D>(qs, r0, dt, l16, lg), dk[dt]);
+            }
         }
     }
 
