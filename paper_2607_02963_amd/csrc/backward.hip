@@ -46,7 +46,7 @@ int launch(const pdec::BwdArgs& a, hipStream_t s)
     hipLaunchKernelGGL((pdec::bwd_dkdv_kernel<D>), dim3(units, a.H_kv), dim3(256), 0, s, a);
     if (hipGetLastError() != hipSuccess) return PDEC_ERR_HIP;
     const long R = (long)a.E * a.N * a.G;
-    hipLaunchKernelGGL((pdec::bwd_dq_kernel<D>), dim3((unsigned)((R + 63) / 64), a.H_kv), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((pdec::bwd_dq_kernel<D>), dim3((unsigned)((R + 63) / 64), a.H_kv), dim3(512), 0, s, a);
     return hipGetLastError() == hipSuccess ? PDEC_OK : PDEC_ERR_HIP;
 }
 

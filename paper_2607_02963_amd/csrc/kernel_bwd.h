@@ -22,8 +22,9 @@
 //     A operand (keys x rows) of dV += P^T dO and dK += dS^T Q; their B
 //     operands (rows x d) come from the row tiles with the transposing LDS
 //     read.  Every key of the unit is written once (0 where no row sees it);
-//  3. dq: one work-group per 64 rows and kv head; wave w holds rows
-//     16w .. 16w + 15 as the B operands of S^T = K Q^T and dP^T = V dO^T, and
+//  3. dq: one work-group per 64 rows and kv head (eight waves: each 16-row
+//     block is held by two waves that split each key tile); a wave holds its
+//     16 rows as the B operands of S^T = K Q^T and dP^T = V dO^T, and
 //     loops over 64-key tiles (prefix, then the own rows of its rows'
 //     streams) staged through LDS.  The S^T accumulator gives a lane row
 //     l % 16 for keys 4(l/16) .. +3, the A operand (rows x keys) of
@@ -280,17 +281,22 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(BwdArgs a)
 }
 
 // ---- 3: dq per 64 rows ----
+// Eight waves: wave w takes rows 16 (w % 4) .. +15 of the 64 and the 16-key
+// blocks 2 (w / 4) and 2 (w / 4) + 1 of each 64-key tile; the two waves of a
+// row block add their dq through LDS at the end.
 template <int D>
-__global__ __launch_bounds__(256) void bwd_dq_kernel(BwdArgs a)
+__global__ __launch_bounds__(512) void bwd_dq_kernel(BwdArgs a)
 {
     constexpr int KS = D / 32;
     constexpr int DT = D / 16;
     constexpr int CH = D / 8;
-    constexpr int PER = 64 * CH / 256;  // staged chunks per thread and tile (K or V)
-    __shared__ __attribute__((aligned(16))) unsigned char ks[64 * 2 * D];
-    __shared__ __attribute__((aligned(16))) unsigned char vs[64 * 2 * D];
+    constexpr int PER = 64 * CH / 512;  // staged chunks per thread and tile (K or V)
+    __shared__ __attribute__((aligned(16))) unsigned char lds[2 * 64 * 2 * D];
+    unsigned char* ks = lds;                // K tile [64][D]
+    unsigned char* vs = lds + 64 * 2 * D;  // V tile [64][D]
 
-    const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, l16 = lane & 15, lg = lane >> 4;
+    const int tid = threadIdx.x, lane = tid & 63, l16 = lane & 15, lg = lane >> 4;
+    const int w = (tid >> 6) & 3, kh = tid >> 8;  // row block, key half
     const int g = blockIdx.y;
     const int R = a.E * a.N * a.G;
     const int L = min(max(a.prefix_len[0], 0), a.Lmax);
@@ -349,7 +355,7 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(BwdArgs a)
         tile_of(t, f, t0, nv);
 #pragma unroll
         for (int m = 0; m < PER; ++m) {
-            const int c = tid + 256 * m, kr = c / CH, ch = c % CH;
+            const int c = tid + 512 * m, kr = c / CH, ch = c % CH;
             kv[m] = vv[m] = u32x4_t{0u, 0u, 0u, 0u};
             if (kr < nv) {
                 const long base = f < 0 ? ((long)(t0 + kr) * a.H_kv + g) * D
@@ -368,7 +374,7 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(BwdArgs a)
         __syncthreads();  // the previous tile is no longer read
 #pragma unroll
         for (int m = 0; m < PER; ++m) {
-            const int c = tid + 256 * m, kr = c / CH, ch = c % CH;
+            const int c = tid + 512 * m, kr = c / CH, ch = c % CH;
             *reinterpret_cast<u32x4_t*>(ks + tile_off<D>(kr, ch)) = kv[m];
             *reinterpret_cast<u32x4_t*>(vs + tile_off<D>(kr, ch)) = vv[m];
         }
@@ -376,7 +382,7 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(BwdArgs a)
         if (t + 1 < tiles) fetch(t + 1, kv, vv);  // next tile, in flight meanwhile
 
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb) {
+        for (int kb = 2 * kh; kb < 2 * kh + 2; ++kb) {
             // S^T = K Q^T, dP^T = V dO^T: lane holds keys 16 kb + 4 lg + i of row l16
             f32x4_t s = {0.f, 0.f, 0.f, 0.f}, dp = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -400,6 +406,19 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(BwdArgs a)
             for (int dt = 0; dt < DT; ++dt) acc[dt] = mfma_16x16x16(dsa, tile_tr<D>(ks, 16 * kb, dt, l16, lg), acc[dt]);
         }
     }
+
+    // the second key half hands its sums to the first through LDS
+    f32x4_t* mbuf = reinterpret_cast<f32x4_t*>(lds);  // [4 row blocks][64 lanes][DT]
+    static_assert(4 * 64 * DT * 16 <= 2 * 64 * 2 * D, "merge buffer");
+    __syncthreads();  // the tiles are no longer read
+    if (kh == 1) {
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) mbuf[(w * 64 + lane) * DT + dt] = acc[dt];
+    }
+    __syncthreads();
+    if (kh == 1) return;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) acc[dt] += mbuf[(w * 64 + lane) * DT + dt];
 
     // lane holds rows 16 w + 4 lg + i, d = 16 dt + l16
 #pragma unroll
