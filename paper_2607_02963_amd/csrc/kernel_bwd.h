@@ -25,7 +25,7 @@
 //  3. dq: one work-group per 64 rows and kv head (eight waves: each 16-row
 //     block is held by two waves that split each key tile); a wave holds its
 //     16 rows as the B operands of S^T = K Q^T and dP^T = V dO^T, and
-//     loops over 64-key tiles (prefix, then the own rows of its rows'
+//     loops over 128-key tiles (prefix, then the own rows of its rows'
 //     streams) staged through LDS.  The S^T accumulator gives a lane row
 //     l % 16 for keys 4(l/16) .. +3, the A operand (rows x keys) of
 //     dQ += dS K, whose B operand (keys x d) is the transposing read of the
@@ -281,19 +281,20 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(BwdArgs a)
 }
 
 // ---- 3: dq per 64 rows ----
-// Eight waves: wave w takes rows 16 (w % 4) .. +15 of the 64 and the 16-key
-// blocks 2 (w / 4) and 2 (w / 4) + 1 of each 64-key tile; the two waves of a
-// row block add their dq through LDS at the end.
+// Eight waves: wave w takes rows 16 (w % 4) .. +15 of the 64 and half of the
+// 16-key blocks of each 128-key tile (the first half for w < 4); the two
+// waves of a row block add their dq through LDS at the end.
 template <int D>
 __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdArgs a)
 {
     constexpr int KS = D / 32;
     constexpr int DT = D / 16;
     constexpr int CH = D / 8;
-    constexpr int PER = 64 * CH / 512;  // staged chunks per thread and tile (K or V)
-    __shared__ __attribute__((aligned(16))) unsigned char lds[2 * 64 * 2 * D];
-    unsigned char* ks = lds;                // K tile [64][D]
-    unsigned char* vs = lds + 64 * 2 * D;  // V tile [64][D]
+    constexpr int TK = 128;                  // keys per staged tile
+    constexpr int PER = TK * CH / 512;       // staged chunks per thread and tile (K or V)
+    __shared__ __attribute__((aligned(16))) unsigned char lds[2 * TK * 2 * D];
+    unsigned char* ks = lds;                // K tile [TK][D]
+    unsigned char* vs = lds + TK * 2 * D;  // V tile [TK][D]
 
     const int tid = threadIdx.x, lane = tid & 63, l16 = lane & 15, lg = lane >> 4;
     const int w = (tid >> 6) & 3, kh = tid >> 8;  // row block, key half
@@ -324,23 +325,23 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdArgs a)
 
     // key tiles: the prefix, then the cache rows of the streams of this work-group's rows
     const int f_lo = min(rw0, R - 1) / (a.N * a.G), f_hi = min(rw0 + 63, R - 1) / (a.N * a.G);
-    const int np = (L + 63) / 64;
+    const int np = (L + TK - 1) / TK;
     int tiles = np;
-    for (int f = f_lo; f <= f_hi; ++f) tiles += (max(a.event_lens[f], 0) + 63) / 64;
+    for (int f = f_lo; f <= f_hi; ++f) tiles += (max(a.event_lens[f], 0) + TK - 1) / TK;
     // tile t: (stream or -1, first key, valid keys)
     auto tile_of = [&](int t, int& f, int& t0, int& nv) {
         if (t < np) {
             f = -1;
-            t0 = 64 * t;
-            nv = min(64, L - t0);
+            t0 = TK * t;
+            nv = min(TK, L - t0);
             return;
         }
         t -= np;
         for (f = f_lo; f <= f_hi; ++f) {
-            const int nf = max(a.event_lens[f], 0), nt = (nf + 63) / 64;
+            const int nf = max(a.event_lens[f], 0), nt = (nf + TK - 1) / TK;
             if (t < nt) {
-                t0 = 64 * t;
-                nv = min(64, nf - t0);
+                t0 = TK * t;
+                nv = min(TK, nf - t0);
                 return;
             }
             t -= nt;
@@ -349,7 +350,7 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdArgs a)
         t0 = 0;
         nv = 0;  // not reached: t < tiles
     };
-    // staging: thread tid moves chunks tid + 256 m of the tile's 64 x CH (K and V)
+    // staging: thread tid moves chunks tid + 512 m of the tile's TK x CH (K and V)
     auto fetch = [&](int t, u32x4_t (&kv)[PER], u32x4_t (&vv)[PER]) {
         int f, t0, nv;
         tile_of(t, f, t0, nv);
@@ -382,7 +383,7 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdArgs a)
         if (t + 1 < tiles) fetch(t + 1, kv, vv);  // next tile, in flight meanwhile
 
 #pragma unroll
-        for (int kb = 2 * kh; kb < 2 * kh + 2; ++kb) {
+        for (int kb = (TK / 32) * kh; kb < (TK / 32) * (kh + 1); ++kb) {
             // S^T = K Q^T, dP^T = V dO^T: lane holds keys 16 kb + 4 lg + i of row l16
             f32x4_t s = {0.f, 0.f, 0.f, 0.f}, dp = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -409,7 +410,7 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdArgs a)
 
     // the second key half hands its sums to the first through LDS
     f32x4_t* mbuf = reinterpret_cast<f32x4_t*>(lds);  // [4 row blocks][64 lanes][DT]
-    static_assert(4 * 64 * DT * 16 <= 2 * 64 * 2 * D, "merge buffer");
+    static_assert(4 * 64 * DT * 16 <= 2 * TK * 2 * D, "merge buffer");
     __syncthreads();  // the tiles are no longer read
     if (kh == 1) {
 #pragma unroll
