@@ -422,15 +422,13 @@ def run_prefill_backward(args, torch, pdec, wl):
     dK, dQ), 10 * D per visible (row, key) pair; the kernels' recomputation
     of S and dP for dQ is not counted.  µs per call from HIP events around K
     back-to-back calls."""
-    E, N, L, H_q, H_kv, D = 13, 48, 32768, 28, 4, 128
-    rng = np.random.default_rng(8)
+    w = wl.prefill_backward_32k()
+    (E, N, H_q, D), L, H_kv = w.q.shape, w.k_prefix.shape[0], w.k_prefix.shape[1]
 
-    def f(*shape):
-        a = wl.bf16_bits((0.5 * rng.standard_normal(shape, dtype=np.float32)).astype(np.float32))
+    def f(a):
         return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
 
-    q, kp, vp, ke, ve, do = f(E, N, H_q, D), f(L, H_kv, D), f(L, H_kv, D), f(E, N, H_kv, D), f(E, N, H_kv, D), \
-        f(E, N, H_q, D)
+    q, kp, vp, ke, ve, do = (f(a) for a in (w.q, w.k_prefix, w.v_prefix, w.k_event, w.v_event, w.dout))
     lens = torch.full((E,), N, dtype=torch.int32, device="cuda")
     plen = torch.tensor([L], dtype=torch.int32, device="cuda")
     out, lse = pdec.attn_prefill(q, kp, vp, ke, ve, lens, plen)

@@ -68,3 +68,59 @@ def attn_prefill_backward(q, k_prefix, v_prefix, k_event, v_event, event_lens, o
                 dvp[:, g] += p[:L, None] * do
                 dve[e, :own, g] += p[L:, None] * do
     return dq, dkp, dvp, dke, dve
+
+
+def sampled_gradients(q, k_prefix, v_prefix, k_event, v_event, event_lens, out, lse, dout,
+                      rows=(), prefix_keys=(), own_keys=(), scale: float = 0.0):
+    """Selected entries of the same gradients, each formed on its own from
+    the definitions above, for shapes where the full loop is too slow:
+      rows        (e, j, h): dq of that query row over its visible keys;
+      prefix_keys (l, g):    dk, dv of prefix row l of kv head g, summed over
+                             every live query row of the heads of group g;
+      own_keys    (e, t, g): dk, dv of row t of stream e's cache, summed over
+                             the rows of stream e whose token j sees it
+                             (t < n_e and t <= j).
+    Returns (list of dq [D], list of (dk [D], dv [D]) per prefix key, the same
+    per own key), float64."""
+    q, kp, vp, ke, ve = (_widen(x) for x in (q, k_prefix, v_prefix, k_event, v_event))
+    out, dout = _widen(out), _widen(dout)
+    lse = np.asarray(lse, dtype=np.float64)
+    n = np.asarray(event_lens, dtype=np.int64)
+    E, N, H_q, D = q.shape
+    H_kv = kp.shape[1]
+    G = H_q // H_kv
+    tau = scale if scale > 0 else 1.0 / np.sqrt(D)
+
+    dqs = []
+    for e, j, h in rows:
+        if n[e] <= 0:
+            dqs.append(np.zeros(D))
+            continue
+        g, own = h // G, min(j, n[e] - 1) + 1
+        keys = np.concatenate([kp[:, g], ke[e, :own, g]])
+        vals = np.concatenate([vp[:, g], ve[e, :own, g]])
+        p = np.exp(tau * (keys @ q[e, j, h]) - lse[e, j, h])
+        ds = p * (vals @ dout[e, j, h] - dout[e, j, h] @ out[e, j, h])
+        dqs.append(tau * (ds @ keys))
+
+    def key_grads(k, v, qs, dos, outs, lses):
+        # qs, dos, outs [rows, D], lses [rows]: the query rows that see key k
+        p = np.exp(tau * (qs @ k) - lses)
+        ds = p * (dos @ v - np.einsum("rd,rd->r", dos, outs))
+        return tau * (ds @ qs), p @ dos
+
+    live = n > 0
+    pks = []
+    for l, g in prefix_keys:
+        sl = (live, slice(None), slice(g * G, (g + 1) * G))
+        pks.append(key_grads(kp[l, g], vp[l, g], q[sl].reshape(-1, D), dout[sl].reshape(-1, D),
+                             out[sl].reshape(-1, D), lse[sl].reshape(-1)))
+    oks = []
+    for e, t, g in own_keys:
+        if t >= n[e]:
+            oks.append((np.zeros(D), np.zeros(D)))
+            continue
+        sl = (e, slice(t, N), slice(g * G, (g + 1) * G))
+        oks.append(key_grads(ke[e, t, g], ve[e, t, g], q[sl].reshape(-1, D), dout[sl].reshape(-1, D),
+                             out[sl].reshape(-1, D), lse[sl].reshape(-1)))
+    return dqs, pks, oks

@@ -389,3 +389,36 @@ def aggregation_32k(seed: int = 6) -> AggregationInputs:
     sizes[-1] += 32704 - int(sizes.sum())
     return make_aggregation(name="aggregation_N32704_S128_K32_H3584", K=32, N=32704, S=128, hidden=3584, H_q=28,
                             H_kv=4, D=128, seed=seed, sizes=sizes, empty_events=1)
+
+
+@dataclass
+class PrefillBackwardInputs:
+    """Whole-branch attention backward: E branches of N tokens over an
+    L-token prefix, bf16 bit patterns.  Every branch is whole (n_e = N) and
+    its cache holds exactly its N rows."""
+    name: str
+    q: np.ndarray          # [E, N, H_q, D] uint16
+    k_prefix: np.ndarray   # [L, H_kv, D]
+    v_prefix: np.ndarray
+    k_event: np.ndarray    # [E, N, H_kv, D]
+    v_event: np.ndarray
+    dout: np.ndarray       # [E, N, H_q, D]
+    event_lens: np.ndarray  # [E] int32
+    seed: int
+
+
+def prefill_backward_32k(seed: int = 8) -> PrefillBackwardInputs:
+    """13 branches x 48 tokens over a 32768-token prefix (H 28/4, D 128):
+    about 13 subchains of about 42 tokens per video (App. B) over the long
+    prefix of the decode workload.  N(0, 1) * 0.5 float32 draws in the order
+    q, k_prefix, v_prefix, k_event, v_event, dout, rounded to bf16."""
+    E, N, L, H_q, H_kv, D = 13, 48, 32768, 28, 4, 128
+    rng = np.random.default_rng(seed)
+
+    def f(*shape):
+        return bf16_bits((0.5 * rng.standard_normal(shape, dtype=np.float32)).astype(np.float32))
+
+    q, kp, vp, ke, ve, do = f(E, N, H_q, D), f(L, H_kv, D), f(L, H_kv, D), f(E, N, H_kv, D), f(E, N, H_kv, D), \
+        f(E, N, H_q, D)
+    return PrefillBackwardInputs("prefill_backward_L32768_E13_N48", q, kp, vp, ke, ve, do,
+                                 np.full(E, N, np.int32), seed)

@@ -86,3 +86,37 @@ def test_backward_cache_longer_than_branch_and_repeatable():
     b = _run_and_check(c)
     for x, y in zip(a, b):
         assert np.array_equal(x, y)
+
+
+def test_backward_32k_sampled_entries():
+    """The bench's workload (13 branches x 48 tokens over a 32768-token
+    prefix, H 28/4, D 128), in the bench's launch: sampled dq rows, and dk, dv
+    of sampled prefix and cache rows, against the oracle's per-entry form,
+    each kind held to the bf16 bar over its samples."""
+    w = wl.prefill_backward_32k()
+    E, N, H_q, D = w.q.shape
+    L, H_kv = w.k_prefix.shape[:2]
+    d = {k: dev_float(getattr(w, k), "bf16") for k in ("q", "k_prefix", "v_prefix", "k_event", "v_event", "dout")}
+    n, plen = dev_int(w.event_lens), dev_int([L])
+    out, lse = pdec.attn_prefill(d["q"], d["k_prefix"], d["v_prefix"], d["k_event"], d["v_event"], n, plen)
+    grads = pdec.attn_prefill_backward(d["q"], d["k_prefix"], d["v_prefix"], d["k_event"], d["v_event"], n, plen,
+                                       out, lse, d["dout"])
+    torch.cuda.synchronize()
+    got = [g.cpu().numpy() for g in grads]
+    out_h = out.cpu().view(torch.int16).numpy().view(np.uint16).reshape(E, N, H_q, D)
+    lse_h = lse.cpu().numpy().reshape(E, N, H_q)
+
+    rng = np.random.default_rng(81)
+    rows = [(0, 0, 0), (E - 1, N - 1, H_q - 1), (5, 17, 13)] + \
+        [tuple(int(rng.integers(0, s)) for s in (E, N, H_q)) for _ in range(9)]
+    pkeys = [(0, 0), (L - 1, H_kv - 1), (63, 1), (64, 2)] + \
+        [(int(rng.integers(0, L)), int(rng.integers(0, H_kv))) for _ in range(12)]
+    okeys = [(0, 0, 0), (E - 1, N - 1, H_kv - 1), (3, 31, 2)] + \
+        [tuple(int(rng.integers(0, s)) for s in (E, N, H_kv)) for _ in range(9)]
+    dqs, pks, oks = backward.sampled_gradients(w.q, w.k_prefix, w.v_prefix, w.k_event, w.v_event, w.event_lens,
+                                               out_h, lse_h, w.dout, rows, pkeys, okeys)
+    _close(np.stack([got[0][r] for r in rows]), np.stack(dqs), "dq")
+    _close(np.stack([got[1][k] for k in pkeys]), np.stack([a for a, _ in pks]), "dk_prefix")
+    _close(np.stack([got[2][k] for k in pkeys]), np.stack([b for _, b in pks]), "dv_prefix")
+    _close(np.stack([got[3][k] for k in okeys]), np.stack([a for a, _ in oks]), "dk_event")
+    _close(np.stack([got[4][k] for k in okeys]), np.stack([b for _, b in oks]), "dv_event")

@@ -115,7 +115,8 @@ def test_backward_oracle_pin(pin):
 
 
 MUTANTS = {
-    "lse_added": ("- lse[e, j, h])", "+ lse[e, j, h])"),
+    "lse_added": ("                p = np.exp(tau * (keys @ q[e, j, h]) - lse[e, j, h])",
+                  "                p = np.exp(tau * (keys @ q[e, j, h]) + lse[e, j, h])"),
     "no_row_term": ("ds = p * (vals @ do - do @ out[e, j, h])", "ds = p * (vals @ do)"),
     "head_group_modulo": ("                g = h // G\n", "                g = h % H_kv\n"),
     "own_rows_one_more": ("own = min(j, n[e] - 1) + 1", "own = min(j + 1, n[e]) + 1"),
@@ -143,3 +144,29 @@ def test_backward_pins_reject_mutant(name, tmp_path):
         except Exception:
             failed += 1
     assert failed > 0, f"every pin passed on mutant {name}"
+
+
+@pytest.mark.parametrize("seed,n", [(11, (3, 0, 2)), (12, (1, 3, 3))])
+def test_sampled_gradients_agree_with_the_full_loop(seed, n):
+    """The per-entry form (each dq row over its keys; each key's dk, dv over
+    the rows that see it) gives every entry of the full loop, which the pins
+    above tie to finite differences: ended streams, rows past n_e and cache
+    rows nobody sees included."""
+    c = _case(seed, E=3, N=4, L=5, n=n, H_q=4, H_kv=2, D=4, cap=4)
+    full = _grads(backward, c)
+    out, lse = _forward(c)
+    E, N, H_q = c["q"].shape[:3]
+    L, H_kv = c["kp"].shape[:2]
+    rows = [(e, j, h) for e in range(E) for j in range(N) for h in range(H_q)]
+    pkeys = [(l, g) for l in range(L) for g in range(H_kv)]
+    okeys = [(e, t, g) for e in range(E) for t in range(4) for g in range(H_kv)]
+    dqs, pks, oks = backward.sampled_gradients(c["q"], c["kp"], c["vp"], c["ke"], c["ve"], c["n"], out, lse,
+                                               c["do"], rows, pkeys, okeys)
+    for (e, j, h), got in zip(rows, dqs):
+        np.testing.assert_allclose(got, full[0][e, j, h], atol=1e-12)
+    for (l, g), (dk, dv) in zip(pkeys, pks):
+        np.testing.assert_allclose(dk, full[1][l, g], atol=1e-12)
+        np.testing.assert_allclose(dv, full[2][l, g], atol=1e-12)
+    for (e, t, g), (dk, dv) in zip(okeys, oks):
+        np.testing.assert_allclose(dk, full[3][e, t, g], atol=1e-12)
+        np.testing.assert_allclose(dv, full[4][e, t, g], atol=1e-12)
