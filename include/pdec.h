@@ -207,6 +207,27 @@ int pdec_set_path(int path);
  */
 int pdec_query_plan(const pdec_dims* dims, int32_t num_videos, int32_t* path, int32_t* chunk_keys);
 
+/* The whole work split of a step call, for tests and measurement. */
+typedef struct pdec_plan_info {
+    int32_t path;          /* 1 = vector kernel, 2 = matrix-core kernel                          */
+    int32_t kernel_shape;  /* matrix-core work-group shape: 1 = 64 rows, 2 = 128 rows,          */
+                           /* 3 = 256 rows; 0 on the vector path                                 */
+    int32_t rows_per_item; /* query rows of one kv head that one work item serves               */
+    int32_t row_groups;    /* work items per (video, kv head, chunk): ceil(rows / rows_per_item)  */
+    int32_t chunk_keys;    /* keys of the virtual key sequence per chunk                         */
+    int32_t max_chunks;    /* chunk slots per (video, kv head)                                   */
+    int32_t work_items;    /* work items of the split pass                                       */
+    int32_t merge_pass;    /* 1 if partial states are merged after the split pass, else 0 (the  */
+                           /* split pass writes out and lse itself)                              */
+} pdec_plan_info;
+
+/*
+ * Fills *info with the plan a step call with these dims would use
+ * (num_videos = 1 for pdec_attn_step).  Host-only.  Returns a pdec_status;
+ * PDEC_ERR_INVALID_ARG for a NULL info or invalid dims.
+ */
+int pdec_describe_plan(const pdec_dims* dims, int32_t num_videos, pdec_plan_info* info);
+
 /*
  * Measurement hook.  With n > 0, the i-th step call made after this call
  * brackets its split pass (the kernel that reads the shared prefix and the

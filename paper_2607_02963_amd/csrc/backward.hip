@@ -19,7 +19,8 @@ int check_dims(const pdec_dims* d)
         d->max_prefix_len < 0 || d->queries_per_stream < 0)
         return PDEC_ERR_INVALID_ARG;
     if (d->num_q_heads % d->num_kv_heads != 0) return PDEC_ERR_INVALID_ARG;
-    if (!(d->softmax_scale >= 0.f) || !std::isfinite(d->softmax_scale)) return PDEC_ERR_INVALID_ARG;
+    // as for the forward: a scale <= 0 selects 1/sqrt(D); a positive one must be finite
+    if (!(d->softmax_scale <= 0.f) && !std::isfinite(d->softmax_scale)) return PDEC_ERR_INVALID_ARG;
     if (d->dtype != PDEC_DTYPE_BF16 || (d->head_dim != 64 && d->head_dim != 128)) return PDEC_ERR_UNSUPPORTED;
     if (d->plan_mask != 0 || d->cross_causal != 0) return PDEC_ERR_UNSUPPORTED;
     const long N = d->queries_per_stream > 0 ? d->queries_per_stream : 1;

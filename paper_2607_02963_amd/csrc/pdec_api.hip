@@ -407,4 +407,21 @@ int pdec_query_plan(const pdec_dims* dims, int32_t num_videos, int32_t* path, in
     return PDEC_OK;
 }
 
+int pdec_describe_plan(const pdec_dims* dims, int32_t num_videos, pdec_plan_info* info)
+{
+    if (!info) return PDEC_ERR_INVALID_ARG;
+    const int rc = validate_dims(dims, num_videos);
+    if (rc != PDEC_OK) return rc;
+    const Plan p = make_plan(dims, num_videos);
+    info->path = p.path;
+    info->kernel_shape = p.path == kPathMfma ? p.shape : 0;
+    info->rows_per_item = p.rows_per_item;
+    info->row_groups = p.rg_max;
+    info->chunk_keys = p.unit_per_chunk * kUnitKeys;
+    info->max_chunks = p.max_chunks;
+    info->work_items = (int32_t)std::min<long>(p.n_items, INT32_MAX);
+    info->merge_pass = (p.path == kPathMfma && p.max_chunks == 1) ? 0 : 1;
+    return PDEC_OK;
+}
+
 }  // extern "C"

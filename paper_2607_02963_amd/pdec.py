@@ -27,7 +27,7 @@ PATH_AUTO, PATH_VALU, PATH_MFMA = 0, 1, 2
 
 EXPORTED = ("pdec_strerror", "pdec_workspace_size", "pdec_attn_step", "pdec_attn_step_ragged",
             "pdec_kv_append", "pdec_rope_kv_append", "pdec_set_path", "pdec_query_plan",
-            "pdec_set_split_timer", "pdec_grounding_workspace_size", "pdec_segment_grounding",
+            "pdec_set_split_timer", "pdec_describe_plan", "pdec_grounding_workspace_size", "pdec_segment_grounding",
             "pdec_aggregation_workspace_size", "pdec_aggregate", "pdec_backward_workspace_size",
             "pdec_attn_prefill_backward")
 
@@ -44,6 +44,14 @@ class Dims(ctypes.Structure):
                 ("softmax_scale", ctypes.c_float), ("prefix_tokens", ctypes.c_int64),
                 ("plan_mask", ctypes.c_int32), ("plan_tokens_per_stream", ctypes.c_int32),
                 ("queries_per_stream", ctypes.c_int32), ("cross_causal", ctypes.c_int32)]
+
+
+class PlanInfo(ctypes.Structure):
+    """Mirror of ``pdec_plan_info``."""
+
+    _fields_ = [("path", ctypes.c_int32), ("kernel_shape", ctypes.c_int32), ("rows_per_item", ctypes.c_int32),
+                ("row_groups", ctypes.c_int32), ("chunk_keys", ctypes.c_int32), ("max_chunks", ctypes.c_int32),
+                ("work_items", ctypes.c_int32), ("merge_pass", ctypes.c_int32)]
 
 
 class GroundDims(ctypes.Structure):
@@ -115,6 +123,8 @@ def lib():
         L.pdec_set_path.argtypes = [ctypes.c_int]
         L.pdec_query_plan.restype = ctypes.c_int
         L.pdec_query_plan.argtypes = [dp, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)]
+        L.pdec_describe_plan.restype = ctypes.c_int
+        L.pdec_describe_plan.argtypes = [dp, i32, ctypes.POINTER(PlanInfo)]
         L.pdec_set_split_timer.restype = ctypes.c_int
         L.pdec_set_split_timer.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int]
         _lib = L
@@ -175,6 +185,13 @@ def query_plan(dims: Dims, num_videos: int = 1):
     _check("pdec_query_plan", lib().pdec_query_plan(ctypes.byref(dims), int(num_videos), ctypes.byref(path),
                                                     ctypes.byref(chunk)))
     return path.value, chunk.value
+
+
+def describe_plan(dims: Dims, num_videos: int = 1) -> dict:
+    """The whole work split of a step call (``pdec_describe_plan``) as a dict."""
+    info = PlanInfo()
+    _check("pdec_describe_plan", lib().pdec_describe_plan(ctypes.byref(dims), int(num_videos), ctypes.byref(info)))
+    return {name: getattr(info, name) for name, _ in PlanInfo._fields_}
 
 
 def set_path(path: int) -> int:

@@ -194,3 +194,28 @@ def test_backward_dims_checks():
     args = [p] * 15
     assert pdec.lib().pdec_attn_prefill_backward(ctypes.byref(ok), *args, ws, ctypes.c_size_t(16), None) \
         == pdec.PDEC_ERR_WORKSPACE
+
+
+def test_non_positive_scale_selects_the_default_in_forward_and_backward():
+    """One dims struct serves the forward and the backward: a scale <= 0
+    selects 1/sqrt(D) in both, a non-finite positive one is refused by both."""
+    for scale, ok in ((-1.0, True), (0.0, True), (0.125, True), (float("inf"), False), (float("nan"), False)):
+        d = pdec.make_dims(13, 28, 4, 128, 48, 32768, pdec.PDEC_DTYPE_BF16, scale=scale, queries_per_stream=48)
+        assert (pdec.workspace_size(d) > 0) == ok, scale
+        assert (pdec.lib().pdec_backward_workspace_size(ctypes.byref(d)) > 0) == ok, scale
+
+
+def test_describe_plan_matches_query_plan_and_shapes():
+    """pdec_describe_plan agrees with pdec_query_plan and names the
+    matrix-core work-group shape by the rows of one kv head (G = 7)."""
+    expect = {7: (1, 64, 1), 16: (2, 128, 1), 32: (3, 256, 1), 64: (3, 256, 2), 2: (0, 8, 2)}
+    for E, (shape, rows, groups) in expect.items():
+        d = _dims(num_events=E, max_prefix_len=1100, cap=70)
+        info = pdec.describe_plan(d)
+        path, chunk = pdec.query_plan(d)
+        assert (info["path"], info["chunk_keys"]) == (path, chunk)
+        assert (info["kernel_shape"], info["rows_per_item"], info["row_groups"]) == (shape, rows, groups), (E, info)
+        assert info["work_items"] == info["max_chunks"] * info["row_groups"] * 4
+    with pytest.raises(pdec.PdecError):
+        pdec.describe_plan(_dims(H_q=27))
+    assert pdec.lib().pdec_describe_plan(ctypes.byref(_dims()), 1, None) == pdec.PDEC_ERR_INVALID_ARG

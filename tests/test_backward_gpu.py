@@ -1,18 +1,24 @@
 """Backward pass of the whole-branch attention on the GPU
 (pdec_attn_prefill_backward) against the oracle (oracle/backward.py).
 
-Both take the same inputs: the GPU forward's out (bf16) and lse, and a
-seeded dout.  The kernel meets the matrix cores with P and ds rounded to
-bf16, as the forward does with P; the bar is the bf16 one of the forward,
-taken relative to each gradient's scale: normwise relative error <= 1e-2 and
-max-abs error <= 2e-2 x max |gradient|.  Cache rows no query sees must be
-exactly 0, and an ended stream's dq exactly 0.
+Parity proper: both backward paths take the same out and lse, and neither
+comes from the library.  They are the oracle forward's (oracle.attn_prefill,
+float64), out rounded to bf16 (the kernel's input type) and lse to float32,
+with a seeded dout.  A separate end-to-end check runs the GPU forward then
+the GPU backward against the oracle forward then the oracle backward.
+
+The kernel meets the matrix cores with P and ds rounded to bf16, as the
+forward does with P; the bar is the bf16 one of the forward, taken relative
+to each gradient's scale: normwise relative error <= 1e-2 and max-abs error
+<= 2e-2 x max |gradient|.  Cache rows no query sees must be exactly 0, and an
+ended stream's dq exactly 0.
 """
 import numpy as np
 import pytest
 import torch
 
 import backward
+import oracle
 from gpu_util import dev_float, dev_int
 from paper_2607_02963_amd import pdec
 from paper_2607_02963_amd import workloads as wl
@@ -28,6 +34,19 @@ def _case(seed, E, N, L, lens, H_q, H_kv, D, cap=None, sigma=0.5):
                 ve=f(E, cap, H_kv, D), do=f(E, N, H_q, D), n=np.asarray(lens, np.int32), L=L)
 
 
+def _oracle_forward(q, kp, vp, ke, ve, n, L):
+    """out (float64) and lse (float64) of the oracle forward, one video."""
+    E = q.shape[0]
+    return oracle.attn_prefill(q, kp, vp, ke, ve, n, np.array([0, L], np.int32), np.array([0, E], np.int32))
+
+
+def _forward_inputs(out64, lse64):
+    """The oracle forward rounded to what the kernel takes: out in bf16 (bit
+    patterns), lse in float32.  Ended streams' rows keep 0 / -inf."""
+    out_b = wl.bf16_bits(np.nan_to_num(out64, nan=0.0).astype(np.float32))
+    return out_b, lse64.astype(np.float32)
+
+
 def _close(got, ref, what):
     got, ref = got.astype(np.float64), ref.astype(np.float64)
     scale = max(float(np.abs(ref).max()), 1e-30)
@@ -36,23 +55,32 @@ def _close(got, ref, what):
     assert float(np.abs(got - ref).max()) <= 2e-2 * scale, (what, "max-abs", float(np.abs(got - ref).max()), scale)
 
 
-def _run_and_check(c):
-    d = {k: dev_float(c[k], "bf16") for k in ("q", "kp", "vp", "ke", "ve", "do")}
-    n, plen = dev_int(c["n"]), dev_int([c["L"]])
-    out, lse = pdec.attn_prefill(d["q"], d["kp"], d["vp"], d["ke"], d["ve"], n, plen)
-    grads = pdec.attn_prefill_backward(d["q"], d["kp"], d["vp"], d["ke"], d["ve"], n, plen, out, lse, d["do"])
-    torch.cuda.synchronize()
-    got = [g.cpu().numpy() for g in grads]
-    out_h = out.cpu().view(torch.int16).numpy().view(np.uint16)
-    ref = backward.attn_prefill_backward(c["q"], c["kp"], c["vp"], c["ke"], c["ve"], c["n"], out_h,
-                                         lse.cpu().numpy(), c["do"])
-    for name, g, r in zip(("dq", "dk_prefix", "dv_prefix", "dk_event", "dv_event"), got, ref):
-        if r.size:
-            _close(g, r, name)
-    for e, ne in enumerate(c["n"]):
+NAMES = ("dq", "dk_prefix", "dv_prefix", "dk_event", "dv_event")
+
+
+def _check_zeros(got, n):
+    for e, ne in enumerate(n):
         assert np.all(got[3][e, max(ne, 0):] == 0) and np.all(got[4][e, max(ne, 0):] == 0)
         if ne <= 0:
             assert np.all(got[0][e] == 0)
+
+
+def _run_and_check(c):
+    """Both backward paths from the oracle forward's out and lse."""
+    d = {k: dev_float(c[k], "bf16") for k in ("q", "kp", "vp", "ke", "ve", "do")}
+    n, plen = dev_int(c["n"]), dev_int([c["L"]])
+    out64, lse64 = _oracle_forward(c["q"], c["kp"], c["vp"], c["ke"], c["ve"], c["n"], c["L"])
+    out_b, lse_f = _forward_inputs(out64, lse64)
+    out_d = dev_float(out_b, "bf16")
+    lse_d = torch.from_numpy(np.ascontiguousarray(lse_f)).cuda()
+    grads = pdec.attn_prefill_backward(d["q"], d["kp"], d["vp"], d["ke"], d["ve"], n, plen, out_d, lse_d, d["do"])
+    torch.cuda.synchronize()
+    got = [g.cpu().numpy() for g in grads]
+    ref = backward.attn_prefill_backward(c["q"], c["kp"], c["vp"], c["ke"], c["ve"], c["n"], out_b, lse_f, c["do"])
+    for name, g, r in zip(NAMES, got, ref):
+        if r.size:
+            _close(g, r, name)
+    _check_zeros(got, c["n"])
     return got
 
 
@@ -70,6 +98,25 @@ CASES = [
 def test_backward_matches_oracle(case):
     seed, E, N, L, lens, H_q, H_kv, D = case
     _run_and_check(_case(seed, E, N, L, lens, H_q, H_kv, D))
+
+
+def test_forward_then_backward_end_to_end():
+    """GPU forward then GPU backward, against oracle forward (float64, not
+    rounded) then oracle backward: what a training step computes."""
+    c = _case(11, 4, 16, 1000, [16, 16, 9, 0], 28, 4, 128)
+    d = {k: dev_float(c[k], "bf16") for k in ("q", "kp", "vp", "ke", "ve", "do")}
+    n, plen = dev_int(c["n"]), dev_int([c["L"]])
+    out, lse = pdec.attn_prefill(d["q"], d["kp"], d["vp"], d["ke"], d["ve"], n, plen)
+    grads = pdec.attn_prefill_backward(d["q"], d["kp"], d["vp"], d["ke"], d["ve"], n, plen, out, lse, d["do"])
+    torch.cuda.synchronize()
+    got = [g.cpu().numpy() for g in grads]
+    out64, lse64 = _oracle_forward(c["q"], c["kp"], c["vp"], c["ke"], c["ve"], c["n"], c["L"])
+    ref = backward.attn_prefill_backward(c["q"], c["kp"], c["vp"], c["ke"], c["ve"], c["n"],
+                                         np.nan_to_num(out64, nan=0.0), lse64, c["do"])
+    for name, g, r in zip(NAMES, got, ref):
+        if r.size:
+            _close(g, r, name)
+    _check_zeros(got, c["n"])
 
 
 def test_backward_of_causal_attention_over_the_prefix():
@@ -90,21 +137,24 @@ def test_backward_cache_longer_than_branch_and_repeatable():
 
 def test_backward_32k_sampled_entries():
     """The bench's workload (13 branches x 48 tokens over a 32768-token
-    prefix, H 28/4, D 128), in the bench's launch: sampled dq rows, and dk, dv
-    of sampled prefix and cache rows, against the oracle's per-entry form,
-    each kind held to the bf16 bar over its samples."""
+    prefix, H 28/4, D 128), in the bench's launch, from the oracle forward's
+    out and lse (every row: the prefix keys' gradients sum over all of them):
+    sampled dq rows, and dk, dv of sampled prefix and cache rows, against the
+    oracle's per-entry form, each kind held to the bf16 bar over its
+    samples."""
     w = wl.prefill_backward_32k()
     E, N, H_q, D = w.q.shape
     L, H_kv = w.k_prefix.shape[:2]
     d = {k: dev_float(getattr(w, k), "bf16") for k in ("q", "k_prefix", "v_prefix", "k_event", "v_event", "dout")}
     n, plen = dev_int(w.event_lens), dev_int([L])
-    out, lse = pdec.attn_prefill(d["q"], d["k_prefix"], d["v_prefix"], d["k_event"], d["v_event"], n, plen)
+    out64, lse64 = _oracle_forward(w.q, w.k_prefix, w.v_prefix, w.k_event, w.v_event, w.event_lens, L)
+    out_h, lse_h = _forward_inputs(out64, lse64)
+    out_d = dev_float(out_h, "bf16")
+    lse_d = torch.from_numpy(np.ascontiguousarray(lse_h)).cuda()
     grads = pdec.attn_prefill_backward(d["q"], d["k_prefix"], d["v_prefix"], d["k_event"], d["v_event"], n, plen,
-                                       out, lse, d["dout"])
+                                       out_d, lse_d, d["dout"])
     torch.cuda.synchronize()
     got = [g.cpu().numpy() for g in grads]
-    out_h = out.cpu().view(torch.int16).numpy().view(np.uint16).reshape(E, N, H_q, D)
-    lse_h = lse.cpu().numpy().reshape(E, N, H_q)
 
     rng = np.random.default_rng(81)
     rows = [(0, 0, 0), (E - 1, N - 1, H_q - 1), (5, 17, 13)] + \

@@ -1,12 +1,17 @@
-"""Bit-exact masking on the GPU.
+"""Bit-exact masking on the GPU, on every split-kernel shape.
 
 Memory the §3.4 mask hides from a row — other streams' cache rows, cache rows
 at or past n_e, prefix rows past the video's length, other videos' data, the
 workspace and the output buffers' old contents — is filled with NaN or huge
 values; every visible output must stay bitwise identical to the clean run.
 Ended streams must stay exactly 0 / -inf.  Permuting streams (or query heads
-within a group) must permute the outputs bitwise, which also pins the lse
-indexing.
+within a group) must permute the outputs, which also pins the lse indexing.
+
+With 28 query heads over 4 kv heads (G = 7), the stream counts below put
+E*G = 49, 112, 224 and 448 query rows on each kv head: the matrix-core
+kernel's 64-row, 128-row and 256-row work-group shapes, and the 256-row shape
+with two row groups.  Every case asserts the shape it reaches, and runs once
+on the automatic path and once forced onto the vector kernel.
 """
 import numpy as np
 import pytest
@@ -20,6 +25,12 @@ pytestmark = pytest.mark.gpu
 
 BF16_NAN = np.uint16(0x7FC0)
 BF16_BIG = wl.bf16_bits(np.array([1e30], np.float32))[0]
+
+# streams -> (kernel shape, rows per item, row groups) on the matrix-core path
+SHAPES = {7: (1, 64, 1), 16: (2, 128, 1), 32: (3, 256, 1), 64: (3, 256, 2)}
+STREAMS = sorted(SHAPES)
+SIDS = [f"E{e}_rows{SHAPES[e][1]}x{SHAPES[e][2]}" for e in STREAMS]
+CAP = 70
 
 
 @pytest.fixture(autouse=True, params=[pdec.PATH_AUTO, pdec.PATH_VALU], ids=["auto", "valu"])
@@ -37,17 +48,45 @@ def _same(a, b):
     return torch.equal(_bits(a), _bits(b))
 
 
-def _step():
-    return wl.make_step(name="mask", dtype="bf16", prefix_lens=(1100,), events_per_video=(7,),
-                        event_lens=[3, 0, 9, 1, 0, 12, 5], cap=14, seed=31)
+def _lens(E: int) -> list:
+    """Every fifth stream ended; the others span one or two own units (up to
+    the full cache), so own units of several lengths meet every row tile."""
+    rng = np.random.default_rng(1000 + E)
+    n = rng.integers(1, CAP + 1, size=E)
+    n[::5] = 0
+    n[1] = CAP
+    n[2] = 1
+    n[3] = 65
+    return [int(x) for x in n]
 
 
+def _step(E: int):
+    return wl.make_step(name=f"mask_E{E}", dtype="bf16", prefix_lens=(1100,), events_per_video=(E,),
+                        event_lens=_lens(E), cap=CAP, seed=31 + E)
+
+
+def _assert_shape(s, path):
+    """The case runs on the kernel shape it is meant to cover."""
+    dims = pdec.make_dims(s.num_events, s.H_q, s.H_kv, s.D, s.cap, int(s.prefix_lens.max()),
+                          pdec.PDEC_DTYPE_BF16, max_events_per_video=int(s.events_per_video.max()))
+    info = pdec.describe_plan(dims, s.num_videos)
+    if path == pdec.PATH_VALU:
+        assert info["path"] == pdec.PATH_VALU
+        return info
+    shape, rows, groups = SHAPES[s.num_events]
+    assert (info["path"], info["kernel_shape"], info["rows_per_item"], info["row_groups"]) == \
+        (pdec.PATH_MFMA, shape, rows, groups), info
+    return info
+
+
+@pytest.mark.parametrize("E", STREAMS, ids=SIDS)
 @pytest.mark.parametrize("poison", [BF16_NAN, BF16_BIG], ids=["nan", "big"])
-def test_hidden_cache_rows_and_ended_streams_never_read(poison):
-    s = _step()
+def test_hidden_cache_rows_and_ended_streams_never_read(poison, E, path):
+    s = _step(E)
+    _assert_shape(s, path)
     clean = DevStep(s)
     o1, l1 = clean.run()
-    p = _step()
+    p = _step(E)
     for e in range(p.num_events):
         n = p.event_lens[e]
         p.k_event[e, n:] = poison
@@ -60,10 +99,12 @@ def test_hidden_cache_rows_and_ended_streams_never_read(poison):
     check("bf16", host(o1), host(l1), *oracle_ref(s))
 
 
-def test_prefix_rows_past_length_never_read():
+@pytest.mark.parametrize("E", STREAMS, ids=SIDS)
+def test_prefix_rows_past_length_never_read(E, path):
     """Prefix buffers longer than the prefix: the rows past it are zeros in
     one run and NaN in the other (same shapes, so the same work split)."""
-    s = _step()
+    s = _step(E)
+    _assert_shape(s, path)
     L = int(s.prefix_lens[0])
     d = DevStep(s)
     pad = 300
@@ -82,8 +123,10 @@ def test_prefix_rows_past_length_never_read():
     check("bf16", host(o2), host(l2), *oracle_ref(s))
 
 
-def test_output_and_workspace_contents_are_ignored():
-    s = _step()
+@pytest.mark.parametrize("E", STREAMS, ids=SIDS)
+def test_output_and_workspace_contents_are_ignored(E, path):
+    s = _step(E)
+    _assert_shape(s, path)
     d = DevStep(s)
     o1, l1 = d.run()
     out = torch.full_like(o1, float("nan"))
@@ -95,35 +138,50 @@ def test_output_and_workspace_contents_are_ignored():
     assert _same(o1, o2) and _same(l1, l2)
 
 
-def test_other_videos_never_read():
-    s = wl.make_step(name="videos", dtype="bf16", prefix_lens=(600, 900, 300), events_per_video=(4, 3, 5),
-                     own_len_range=(0, 10), seed=5)
+@pytest.mark.parametrize("counts", [(4, 3, 5), (16, 9, 24)], ids=["small", "rows168"])
+def test_other_videos_never_read(counts, path):
+    """A ragged batch: the middle video's prefix, caches and queries are NaN
+    in the second run; the other videos' outputs are bitwise unchanged."""
+    a, b, c = counts
+
+    def make():
+        return wl.make_step(name="videos", dtype="bf16", prefix_lens=(600, 900, 300), events_per_video=counts,
+                            own_len_range=(0, 70), cap=71, seed=5)
+
+    s = make()
     o1, l1 = DevStep(s).run()
-    p = wl.make_step(name="videos", dtype="bf16", prefix_lens=(600, 900, 300), events_per_video=(4, 3, 5),
-                     own_len_range=(0, 10), seed=5)
+    p = make()
     p.k_prefix[600:1500] = BF16_NAN
     p.v_prefix[600:1500] = BF16_NAN
-    p.k_event[4:7] = BF16_NAN
-    p.v_event[4:7] = BF16_NAN
-    p.q[4:7] = BF16_NAN
+    p.k_event[a:a + b] = BF16_NAN
+    p.v_event[a:a + b] = BF16_NAN
+    p.q[a:a + b] = BF16_NAN
     o2, l2 = DevStep(p).run()
     torch.cuda.synchronize()
-    keep = np.r_[0:4, 7:12]
+    keep = np.r_[0:a, a + b:a + b + c]
     assert _same(o1[keep], o2[keep]) and _same(l1[keep], l2[keep])
-    assert torch.isnan(o2[4:7].float()).all()
+    assert torch.isnan(o2[a:a + b].float()).all()
+    check("bf16", host(o1), host(l1), *oracle_ref(s))
 
 
-def test_stream_permutation_permutes_outputs():
+@pytest.mark.parametrize("E", STREAMS, ids=SIDS)
+def test_stream_permutation_permutes_outputs(E, path):
     """Permuting streams permutes the rows.  Each stream's own rows are placed
     by the work split after the streams before it, so the chunks a row's keys
     fall into, its fp32 summation order and the bf16 rounding of its stored
     chunk outputs may change with the permutation: equal to within two bf16
     units in the last place of the largest output (one for the output's own
-    rounding, one for the chunk outputs')."""
-    s = _step()
+    rounding, one for the chunk outputs').  For lse: a row's normaliser is a
+    float32 sum of its n visible keys' bf16-rounded weights, whose rounding
+    depends on the chunk's reference max; each run is within
+    2^-9 + n 2^-24 of the exact ln-normaliser, so the two within twice that.
+    (Which row an lse lands at is pinned exactly by
+    test_lse_lands_at_its_own_index.)"""
+    s = _step(E)
+    _assert_shape(s, path)
     o1, l1 = DevStep(s).run()
-    perm = np.array([5, 2, 6, 0, 3, 1, 4])
-    p = _step()
+    perm = np.random.default_rng(E).permutation(E)
+    p = _step(E)
     p.q, p.k_event, p.v_event, p.event_lens = s.q[perm], s.k_event[perm], s.v_event[perm], s.event_lens[perm]
     o2, l2 = DevStep(p).run()
     torch.cuda.synchronize()
@@ -134,29 +192,32 @@ def test_stream_permutation_permutes_outputs():
     ulp = 2.0 ** (np.floor(np.log2(top)) - 7)  # bf16 spacing at the largest output
     assert (a - b).abs().max().item() <= 2 * ulp
     live = ~torch.isneginf(l2)
-    assert (l1[pt][live] - l2[live]).abs().max().item() <= 1e-5
+    n_keys = int(s.prefix_lens[0]) + int(s.event_lens.max())
+    assert (l1[pt][live] - l2[live]).abs().max().item() <= 2 * (2.0 ** -9 + n_keys * 2.0 ** -24)
 
 
-def test_lse_lands_at_its_own_index():
-    """Every (stream, head) row gets a planted key whose score differs from
-    every other row's by >= 0.5, so its lse is unique to it: a row written
-    at any other index would miss the oracle by far more than the
+@pytest.mark.parametrize("E", STREAMS, ids=SIDS)
+def test_lse_lands_at_its_own_index(E, path):
+    """Every (stream, head) row gets a planted prefix key score of its own,
+    40 tau (8 + row / 16), with row = e * H_q + h: q's first two coordinates
+    carry 8 + row // 16 and (row % 16) / 16, both exact in bf16, and one
+    prefix key per kv head is 40 on those two coordinates.  That score (>= 28)
+    dominates the row, so lses of different rows differ by >= 0.2: a row
+    written at any other index misses the oracle by far more than the
     tolerance."""
-    s = wl.make_step(name="lse_index", dtype="bf16", prefix_lens=(700,), events_per_video=(5,),
-                     event_lens=[2, 4, 0, 1, 3], cap=4, seed=41)
-    D = s.D
+    s = _step(E)
+    _assert_shape(s, path)
     q = wl.bf16_widen(s.q)
-    # one prefix key per kv head, aligned with a fixed direction; each query
-    # row gets a different projection onto that direction
-    u = np.zeros(D, np.float32)
-    u[0] = 1.0
+    u = np.zeros(s.D, np.float32)
+    u[0] = u[1] = 40.0
     for g in range(s.H_kv):
-        s.k_prefix[g, g] = wl.bf16_bits(40.0 * u)
-    for e in range(5):
+        s.k_prefix[3 * g + 1, g] = wl.bf16_bits(u)
+    for e in range(s.num_events):
         for h in range(s.H_q):
             row = e * s.H_q + h
             qq = q[e, h].copy()
-            qq[0] = (10.0 + 0.5 * row) * np.sqrt(D) / 40.0  # planted score 10 + row/2
+            qq[0] = 8 + row // 16
+            qq[1] = (row % 16) / 16.0
             s.q[e, h] = wl.bf16_bits(qq)
     o, l = DevStep(s).run()
     torch.cuda.synchronize()
@@ -164,17 +225,43 @@ def test_lse_lands_at_its_own_index():
     got = l.cpu().numpy().astype(np.float64)
     live = ~np.isneginf(ref_l)
     vals = np.sort(ref_l[live].ravel())
-    assert np.min(np.diff(vals)) > 0.05  # rows are told apart by their lse
+    assert np.min(np.diff(vals)) > 0.2  # rows are told apart by their lse
     assert np.array_equal(np.isneginf(got), ~live)
     assert np.max(np.abs(got[live] - ref_l[live])) < 0.02
+    check("bf16", host(o), got, ref_o, ref_l)
 
 
-def test_head_permutation_within_groups_permutes_outputs_bitwise():
-    s = _step()
+@pytest.mark.parametrize("E", STREAMS, ids=SIDS)
+def test_planted_peaks_expose_masking(E, path):
+    """Own rows carry keys aligned with their stream's queries (score ~ 30):
+    any leak of another stream's rows, or a dropped own row, is an O(1) error
+    the tolerance cannot hide."""
+    s = _step(E)
+    _assert_shape(s, path)
+    q = wl.bf16_widen(s.q)
+    D = s.D
+    G = s.H_q // s.H_kv
+    for e in range(E):
+        for g in range(s.H_kv):
+            qg = q[e, g * G:(g + 1) * G].mean(axis=0)
+            k = 30.0 * np.sqrt(D) * qg / np.dot(qg, qg)
+            for t in range(s.cap):
+                s.k_event[e, t, g] = wl.bf16_bits(k)
+                s.v_event[e, t, g] = wl.bf16_bits(np.full(D, 0.25 * (e % 8 + 1) + 0.01 * t, np.float32))
+    o, l = DevStep(s).run()
+    torch.cuda.synchronize()
+    st = check("bf16", host(o), host(l), *oracle_ref(s))
+    assert st["out_maxabs"] < 2e-2
+
+
+@pytest.mark.parametrize("E", STREAMS, ids=SIDS)
+def test_head_permutation_within_groups_permutes_outputs_bitwise(E, path):
+    s = _step(E)
+    _assert_shape(s, path)
     o1, l1 = DevStep(s).run()
     G = s.H_q // s.H_kv
     perm = np.concatenate([g * G + np.roll(np.arange(G), 3) for g in range(s.H_kv)])
-    p = _step()
+    p = _step(E)
     p.q = np.ascontiguousarray(s.q[:, perm])
     o2, l2 = DevStep(p).run()
     torch.cuda.synchronize()

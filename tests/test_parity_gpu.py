@@ -1,6 +1,5 @@
 """GPU parity: the HIP path through the C ABI against the CPU oracle on the
-same seeded inputs (element by element at small sizes, sampled rows at the
-full workload sizes)."""
+same seeded inputs, element by element, up to the full workload sizes."""
 import zlib
 
 import numpy as np
@@ -116,15 +115,23 @@ def test_single_8k_workload_full():
     _run_and_check(wl.single_8k())
 
 
-def test_long_32k_workload_sampled_rows():
-    """The headline shape (prefix 32768, 32 streams), sampled rows."""
+def test_long_32k_workload_full():
+    """The headline shape (prefix 32768, 32 streams, own U{0..128}): all 896
+    (stream, head) rows against the oracle."""
+    _run_and_check(wl.long_32k())
+
+
+def test_ragged_16_workload_full():
+    """16 videos, prefixes U{4096..16384}, streams clip(Poisson(12), 4, 24),
+    own U{0..96}: every (stream, head) row against the oracle."""
+    _run_and_check(wl.ragged_16())
+
+
+def test_long_32k_sampled_rows_forced_vector_kernel():
+    """The headline inputs on the vector kernel (forced), sampled rows: the
+    same result from the other split kernel."""
     s = wl.long_32k()
-    _run_and_check(s, sel=sample_rows(s, 96, seed=1))
-
-
-def test_ragged_16_workload_sampled_rows():
-    s = wl.ragged_16()
-    _run_and_check(s, sel=sample_rows(s, 128, seed=2))
+    _run_and_check(s, path=pdec.PATH_VALU, sel=sample_rows(s, 96, seed=1))
 
 
 def test_repeat_runs_are_bitwise_identical():
