@@ -54,7 +54,9 @@ typedef enum {
     PDEC_ERR_INVALID_ARG = -1, /* null / misaligned pointer, inconsistent sizes          */
     PDEC_ERR_UNSUPPORTED = -2, /* a size or type this build has no kernel for (D, dtype) */
     PDEC_ERR_WORKSPACE = -3,   /* workspace smaller than pdec_workspace_size()          */
-    PDEC_ERR_HIP = -4          /* a HIP runtime call or kernel launch failed             */
+    PDEC_ERR_HIP = -4,         /* a HIP runtime call or kernel launch failed             */
+    PDEC_ERR_SCRATCH = -6      /* the step needs more scratch than the library's static  */
+                               /* buffer holds (pdec_attn_step_noalloc only)             */
 } pdec_status;
 
 typedef enum { PDEC_DTYPE_F32 = 0, PDEC_DTYPE_BF16 = 1 } pdec_dtype;
@@ -129,6 +131,28 @@ int pdec_attn_step(const pdec_dims* dims, const void* q, const void* k_prefix, c
                    const void* k_event, const void* v_event, const int32_t* event_lens,
                    const int32_t* prefix_lens, void* out, float* lse, void* workspace,
                    size_t workspace_bytes, void* stream);
+
+/*
+ * pdec_attn_step for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ * Same arguments, semantics and kernels as pdec_attn_step, but the partial
+ * softmax states live in a scratch buffer the library holds in static device
+ * memory: PDEC_NOALLOC_SCRATCH_BYTES (32 MiB) on every GPU the library runs
+ * on, kept until the process ends.  The call allocates and frees nothing
+ * (no hipMalloc / hipFree, no allocating library routine).  A step whose
+ * workspace would exceed the buffer (pdec_workspace_size(dims, 1) >
+ * PDEC_NOALLOC_SCRATCH_BYTES) is refused with PDEC_ERR_SCRATCH before
+ * anything is enqueued.  The prefix 32768 / 32-stream step needs about 15 MiB.
+ * Every call on one GPU shares that GPU's buffer: calls that overlap in time
+ * on one GPU (from several streams or threads) race on it and must be
+ * serialised by the caller.  The first call on a device looks up the
+ * buffer's address there (a host-side query, no allocation).  Returns a
+ * pdec_status.
+ */
+#define PDEC_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+int pdec_attn_step_noalloc(const pdec_dims* dims, const void* q, const void* k_prefix, const void* v_prefix,
+                           const void* k_event, const void* v_event, const int32_t* event_lens,
+                           const int32_t* prefix_lens, void* out, float* lse, void* stream);
 
 /*
  * One parallel decode step over a ragged batch of videos, every (video,

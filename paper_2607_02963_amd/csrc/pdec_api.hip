@@ -16,6 +16,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstdlib>
+#include <mutex>
 #include <type_traits>
 
 #include "pdec.h"
@@ -35,6 +36,30 @@ constexpr int kTargetItems = 256;   // MI355X compute units: one item per CU
 constexpr int kUnitKeys = kUnit;    // keys per unit of the virtual key sequence
 
 std::atomic<int> g_path_override{0};
+
+// Scratch of pdec_attn_step_noalloc: the partial states of one step, in
+// static device memory (one copy per GPU, at its own address there).  Host
+// code never passes the symbol itself to a kernel or a copy: it uses the
+// device address looked up once per device with hipGetSymbolAddress.
+static __device__ __align__(256) unsigned char scratch[PDEC_NOALLOC_SCRATCH_BYTES];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the scratch buffer on the current device (looked up on
+// the first call there); null on failure.
+void* scratch_address()
+{
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_ptr[dev]) {
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return nullptr;
+        g_scratch_ptr[dev] = ptr;
+    }
+    return g_scratch_ptr[dev];
+}
 
 // measurement hook (pdec_set_split_timer)
 void* const* g_timer_start = nullptr;
@@ -281,6 +306,7 @@ const char* pdec_strerror(int status)
     case PDEC_ERR_UNSUPPORTED: return "unsupported size or type (head_dim must be 64 or 128, dtype f32 or bf16)";
     case PDEC_ERR_WORKSPACE: return "workspace smaller than pdec_workspace_size()";
     case PDEC_ERR_HIP: return "HIP runtime error or kernel launch failure";
+    case PDEC_ERR_SCRATCH: return "step needs more scratch than the static buffer of pdec_attn_step_noalloc holds";
     default: return "unknown pdec status";
     }
 }
@@ -298,6 +324,20 @@ int pdec_attn_step(const pdec_dims* dims, const void* q, const void* k_prefix, c
 {
     return run_step(dims, 1, q, k_prefix, v_prefix, nullptr, prefix_lens, k_event, v_event, event_lens, nullptr,
                     out, lse, workspace, workspace_bytes, stream);
+}
+
+int pdec_attn_step_noalloc(const pdec_dims* dims, const void* q, const void* k_prefix, const void* v_prefix,
+                           const void* k_event, const void* v_event, const int32_t* event_lens,
+                           const int32_t* prefix_lens, void* out, float* lse, void* stream)
+{
+    // size check first: nothing touches the device for a refused call
+    const int rc = validate_dims(dims, 1);
+    if (rc != PDEC_OK) return rc;
+    if (make_plan(dims, 1).ws_bytes > PDEC_NOALLOC_SCRATCH_BYTES) return PDEC_ERR_SCRATCH;
+    void* ws = scratch_address();
+    if (!ws) return PDEC_ERR_HIP;
+    return run_step(dims, 1, q, k_prefix, v_prefix, nullptr, prefix_lens, k_event, v_event, event_lens, nullptr,
+                    out, lse, ws, PDEC_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 int pdec_attn_step_ragged(const pdec_dims* dims, int32_t num_videos, const void* q, const void* k_prefix,

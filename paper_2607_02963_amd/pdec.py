@@ -20,12 +20,14 @@ PDEC_ERR_INVALID_ARG = -1
 PDEC_ERR_UNSUPPORTED = -2
 PDEC_ERR_WORKSPACE = -3
 PDEC_ERR_HIP = -4
+PDEC_ERR_SCRATCH = -6
+NOALLOC_SCRATCH_BYTES = 32 << 20
 PDEC_DTYPE_F32 = 0
 PDEC_DTYPE_BF16 = 1
 
 PATH_AUTO, PATH_VALU, PATH_MFMA = 0, 1, 2
 
-EXPORTED = ("pdec_strerror", "pdec_workspace_size", "pdec_attn_step", "pdec_attn_step_ragged",
+EXPORTED = ("pdec_strerror", "pdec_workspace_size", "pdec_attn_step", "pdec_attn_step_noalloc", "pdec_attn_step_ragged",
             "pdec_kv_append", "pdec_rope_kv_append", "pdec_set_path", "pdec_query_plan",
             "pdec_set_split_timer", "pdec_describe_plan", "pdec_grounding_workspace_size", "pdec_segment_grounding",
             "pdec_aggregation_workspace_size", "pdec_aggregate", "pdec_backward_workspace_size",
@@ -99,6 +101,8 @@ def lib():
         L.pdec_workspace_size.argtypes = [dp, i32]
         L.pdec_attn_step.restype = ctypes.c_int
         L.pdec_attn_step.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.pdec_attn_step_noalloc.restype = ctypes.c_int
+        L.pdec_attn_step_noalloc.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
         L.pdec_attn_step_ragged.restype = ctypes.c_int
         L.pdec_attn_step_ragged.argtypes = [dp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         L.pdec_kv_append.restype = ctypes.c_int
@@ -245,6 +249,32 @@ def attn_step(q, k_prefix, v_prefix, k_event, v_event, event_lens, prefix_lens, 
     if event_lens.shape[0] != E or out.shape != q.shape:
         raise ValueError("event_lens / out shape")
     _check("pdec_attn_step", lib().pdec_attn_step(ctypes.byref(dims), *args))
+    return out, lse
+
+
+def attn_step_noalloc(q, k_prefix, v_prefix, k_event, v_event, event_lens, prefix_lens, *, out, lse,
+                      max_prefix_len=None, scale=0.0, stream=None):
+    """``attn_step`` through pdec_attn_step_noalloc: the library's static
+    scratch buffer instead of a workspace, nothing allocated by the call.
+    ``out`` and ``lse`` are the caller's (this wrapper allocates nothing
+    either); returns (out, lse)."""
+    E, H_q, D = q.shape
+    H_kv = k_prefix.shape[1]
+    cap = k_event.shape[1]
+    if max_prefix_len is None:
+        max_prefix_len = k_prefix.shape[0]
+    dims = make_dims(E, H_q, H_kv, D, cap, max_prefix_len, _dtype_code(q), scale)
+    if v_prefix.shape != k_prefix.shape or v_event.shape != k_event.shape or k_event.shape[0] != E:
+        raise ValueError("inconsistent K/V shapes")
+    if k_prefix.shape[2] != D or k_event.shape[3] != D or k_event.shape[2] != H_kv:
+        raise ValueError("head dims disagree")
+    if event_lens.shape[0] != E or out.shape != q.shape or tuple(lse.shape) != (E, H_q):
+        raise ValueError("event_lens / out / lse shape")
+    args = [_dev(q, "q", ndim=3), _dev(k_prefix, "k_prefix", q.dtype, 3), _dev(v_prefix, "v_prefix", q.dtype, 3),
+            _dev(k_event, "k_event", q.dtype, 4), _dev(v_event, "v_event", q.dtype, 4),
+            _dev(event_lens, "event_lens", torch.int32, 1), _dev(prefix_lens, "prefix_lens", torch.int32, 1),
+            _dev(out, "out", q.dtype, 3), _dev(lse, "lse", torch.float32, 2), _stream(stream, q.device)]
+    _check("pdec_attn_step_noalloc", lib().pdec_attn_step_noalloc(ctypes.byref(dims), *args))
     return out, lse
 
 
