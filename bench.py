@@ -531,6 +531,9 @@ def main():
     ap.add_argument("--cross-causal", action="store_true",
                     help="prefill workload: Table 8's 'causal attention' row, each query also seeing the other "
                          "branches' rows at earlier positions")
+    ap.add_argument("--tiles", choices=("16", "32"), default="16",
+                    help="matrix-core tile rows of the decode step: 16 (the automatic choice) or 32 (the 32-row-tile "
+                         "kernel, above 64 query rows per kv head at head_dim 128), for comparing the two")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MB (5 times) and exit; "
                          "used to calibrate the HBM byte counters")
@@ -557,6 +560,8 @@ def main():
     from paper_2607_02963_amd import workloads as wl
 
     torch.cuda.set_device(0)
+    if args.tiles == "32":
+        pdec.set_path(pdec.PATH_MFMA32)
     if args.workload == "loop_64":
         run_loop(args, torch, pdec, wl)
         return

@@ -219,7 +219,9 @@ int pdec_rope_kv_append(const pdec_dims* dims, int32_t num_videos, void* q, cons
  * Kernel-path selection for the shared-prefix pass, for tests and tuning:
  * 0 = automatic (bfloat16 with >= 16 query rows per key/value head uses the
  * matrix-core kernel, everything else the vector kernel), 1 = always the
- * vector kernel, 2 = matrix-core kernel where the type allows it.
+ * vector kernel, 2 = matrix-core kernel where the type allows it, 3 = as 2,
+ * with the decode step at head_dim 128 and more than 64 query rows per kv
+ * head on 32-row tiles (kernel shapes 4 and 5) instead of 16-row ones.
  * Process-wide; returns the previous setting, or PDEC_ERR_INVALID_ARG.
  */
 int pdec_set_path(int path);
@@ -235,7 +237,8 @@ int pdec_query_plan(const pdec_dims* dims, int32_t num_videos, int32_t* path, in
 typedef struct pdec_plan_info {
     int32_t path;          /* 1 = vector kernel, 2 = matrix-core kernel                          */
     int32_t kernel_shape;  /* matrix-core work-group shape: 1 = 64 rows, 2 = 128 rows,          */
-                           /* 3 = 256 rows; 0 on the vector path                                 */
+                           /* 3 = 256 rows on 16-row tiles; 4 = 256 rows, 5 = 128 rows on      */
+                           /* 32-row tiles (pdec_set_path(3) only); 0 on the vector path       */
     int32_t rows_per_item; /* query rows of one kv head that one work item serves               */
     int32_t row_groups;    /* work items per (video, kv head, chunk): ceil(rows / rows_per_item)  */
     int32_t chunk_keys;    /* keys of the virtual key sequence per chunk                         */

@@ -32,6 +32,7 @@ using namespace pdec;
 
 constexpr int kPathValu = 1;
 constexpr int kPathMfma = 2;
+constexpr int kPathMfma32 = 3;  // override only: the decode step's matrix-core path on 32-row tiles
 constexpr int kTargetItems = 256;   // MI355X compute units: one item per CU
 constexpr int kUnitKeys = kUnit;    // keys per unit of the virtual key sequence
 
@@ -130,17 +131,23 @@ Plan make_plan(const pdec_dims* d, int num_videos)
     int path = (d->dtype == PDEC_DTYPE_BF16 && rows_max >= 16) ? kPathMfma : kPathValu;
     const int ov = g_path_override.load();
     if (ov == kPathValu) path = kPathValu;
-    if (ov == kPathMfma && d->dtype == PDEC_DTYPE_BF16) path = kPathMfma;
+    if ((ov == kPathMfma || ov == kPathMfma32) && d->dtype == PDEC_DTYPE_BF16) path = kPathMfma;
     if (qps > 1) path = kPathMfma;  // the vector kernels take one query per stream
     p.path = path;
     if (path == kPathMfma) {
-        // up to 4 tiles -> 8 waves: 1 tile per row wave, 2 key groups (64 rows);
-        // up to 8 -> 8 waves: 2 tiles per row wave, 2 key groups (128 rows);
-        // more -> 256 rows per item: 16 one-tile row waves (decode step,
-        // D = 128) or 8 two-tile row waves (whole branches, D = 64)
+        // up to 4 tiles of 16 rows -> 8 waves: 1 tile per row wave, 2 key
+        // groups (64 rows); up to 8 -> 8 waves: 2 tiles per row wave, 2 key
+        // groups (128 rows); more -> 256 rows per item: 16 one-tile row
+        // waves (decode step, D = 128) or 8 two-tile row waves (whole
+        // branches, D = 64).  On request the decode step at D = 128 with
+        // more than 64 rows runs on 32-row tiles instead (128 rows as 4 row
+        // waves x 2 key groups, 256 rows as 8 row waves): half the LDS
+        // operand reads, but two waves per SIMD, which hide the memory path
+        // worse than four; measured slower at the decode shapes.
         const long tiles = ceil_div(rows_max, 16);
         p.shape = tiles <= 4 ? 1 : tiles <= 8 ? 2 : 3;
         p.rows_per_item = tiles <= 4 ? 64 : tiles <= 8 ? 128 : 256;
+        if (ov == kPathMfma32 && d->head_dim == 128 && qps == 1 && p.shape > 1) p.shape = p.shape == 2 ? 5 : 4;
     } else {
         p.shape = 0;
         p.rows_per_item = 8;
@@ -422,7 +429,7 @@ int pdec_rope_kv_append(const pdec_dims* dims, int32_t num_videos, void* q, cons
 
 int pdec_set_path(int path)
 {
-    if (path < 0 || path > 2) return PDEC_ERR_INVALID_ARG;
+    if (path < 0 || path > kPathMfma32) return PDEC_ERR_INVALID_ARG;
     return g_path_override.exchange(path);
 }
 

@@ -8,6 +8,7 @@
 #include <hip/hip_runtime.h>
 
 #include "kernel_mfma.h"
+#include "kernel_mfma32.h"
 
 namespace pdec {
 
@@ -16,6 +17,18 @@ namespace {
 template <int D, bool PLAN, bool MQ>
 void launch_shape(const StepArgs& a, int shape, int grid, hipStream_t s)
 {
+    if constexpr (D == 128 && !MQ) {
+        // 32-row tiles (decode step at D = 128): 256 rows as eight row waves,
+        // 128 rows as four row waves x two key groups
+        if (shape == 4) {
+            hipLaunchKernelGGL((split_m32_kernel<8, 1, PLAN>), dim3(grid), dim3(512), 0, s, a);
+            return;
+        }
+        if (shape == 5) {
+            hipLaunchKernelGGL((split_m32_kernel<4, 2, PLAN>), dim3(grid), dim3(512), 0, s, a);
+            return;
+        }
+    }
     switch (shape) {
     case 1: hipLaunchKernelGGL((split_mfma_kernel<D, 1, 4, 2, PLAN, MQ>), dim3(grid), dim3(512), 0, s, a); break;
     case 2: hipLaunchKernelGGL((split_mfma_kernel<D, 2, 4, 2, PLAN, MQ>), dim3(grid), dim3(512), 0, s, a); break;

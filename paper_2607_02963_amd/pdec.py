@@ -25,7 +25,7 @@ NOALLOC_SCRATCH_BYTES = 32 << 20
 PDEC_DTYPE_F32 = 0
 PDEC_DTYPE_BF16 = 1
 
-PATH_AUTO, PATH_VALU, PATH_MFMA = 0, 1, 2
+PATH_AUTO, PATH_VALU, PATH_MFMA, PATH_MFMA32 = 0, 1, 2, 3
 
 EXPORTED = ("pdec_strerror", "pdec_workspace_size", "pdec_attn_step", "pdec_attn_step_noalloc", "pdec_attn_step_ragged",
             "pdec_kv_append", "pdec_rope_kv_append", "pdec_set_path", "pdec_query_plan",

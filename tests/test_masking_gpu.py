@@ -9,9 +9,10 @@ within a group) must permute the outputs, which also pins the lse indexing.
 
 With 28 query heads over 4 kv heads (G = 7), the stream counts below put
 E*G = 49, 112, 224 and 448 query rows on each kv head: the matrix-core
-kernel's 64-row, 128-row and 256-row work-group shapes, and the 256-row shape
-with two row groups.  Every case asserts the shape it reaches, and runs once
-on the automatic path and once forced onto the vector kernel.
+kernel's 64-row work-group shape, its 128-row and 256-row shapes on 16-row
+tiles (the automatic choice) and on 32-row tiles, and the 256-row shapes with
+two row groups.  Every case asserts the shape it reaches, and runs on the
+automatic path, on 32-row tiles, and forced onto the vector kernel.
 """
 import numpy as np
 import pytest
@@ -26,14 +27,17 @@ pytestmark = pytest.mark.gpu
 BF16_NAN = np.uint16(0x7FC0)
 BF16_BIG = wl.bf16_bits(np.array([1e30], np.float32))[0]
 
-# streams -> (kernel shape, rows per item, row groups) on the matrix-core path
+# streams -> (kernel shape, rows per item, row groups) on the matrix-core path,
+# automatic (16-row tiles) and on 32-row tiles (above 64 rows)
 SHAPES = {7: (1, 64, 1), 16: (2, 128, 1), 32: (3, 256, 1), 64: (3, 256, 2)}
+SHAPES32 = {7: (1, 64, 1), 16: (5, 128, 1), 32: (4, 256, 1), 64: (4, 256, 2)}
 STREAMS = sorted(SHAPES)
 SIDS = [f"E{e}_rows{SHAPES[e][1]}x{SHAPES[e][2]}" for e in STREAMS]
 CAP = 70
 
 
-@pytest.fixture(autouse=True, params=[pdec.PATH_AUTO, pdec.PATH_VALU], ids=["auto", "valu"])
+@pytest.fixture(autouse=True, params=[pdec.PATH_AUTO, pdec.PATH_MFMA32, pdec.PATH_VALU],
+                ids=["auto", "tile32", "valu"])
 def path(request):
     pdec.set_path(request.param)
     yield request.param
@@ -73,7 +77,7 @@ def _assert_shape(s, path):
     if path == pdec.PATH_VALU:
         assert info["path"] == pdec.PATH_VALU
         return info
-    shape, rows, groups = SHAPES[s.num_events]
+    shape, rows, groups = (SHAPES32 if path == pdec.PATH_MFMA32 else SHAPES)[s.num_events]
     assert (info["path"], info["kernel_shape"], info["rows_per_item"], info["row_groups"]) == \
         (pdec.PATH_MFMA, shape, rows, groups), info
     return info

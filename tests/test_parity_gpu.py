@@ -115,16 +115,19 @@ def test_single_8k_workload_full():
     _run_and_check(wl.single_8k())
 
 
-def test_long_32k_workload_full():
+@pytest.mark.parametrize("path", [pdec.PATH_AUTO, pdec.PATH_MFMA32], ids=["tile16", "tile32"])
+def test_long_32k_workload_full(path):
     """The headline shape (prefix 32768, 32 streams, own U{0..128}): all 896
-    (stream, head) rows against the oracle."""
-    _run_and_check(wl.long_32k())
+    (stream, head) rows against the oracle, on the 256-row 16-row-tile kernel
+    (the automatic choice) and on the 32-row-tile one."""
+    _run_and_check(wl.long_32k(), path=path)
 
 
-def test_ragged_16_workload_full():
+@pytest.mark.parametrize("path", [pdec.PATH_AUTO, pdec.PATH_MFMA32], ids=["tile16", "tile32"])
+def test_ragged_16_workload_full(path):
     """16 videos, prefixes U{4096..16384}, streams clip(Poisson(12), 4, 24),
     own U{0..96}: every (stream, head) row against the oracle."""
-    _run_and_check(wl.ragged_16())
+    _run_and_check(wl.ragged_16(), path=path)
 
 
 def test_long_32k_sampled_rows_forced_vector_kernel():
