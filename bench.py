@@ -9,13 +9,17 @@ Protocol
   * inputs are resident in HBM before timing; several copies of the step's
     inputs (distinct allocations, >= 512 MB together) are cycled so the
     256 MB last-level cache cannot serve the prefix from one step to the next;
-  * W untimed warm-up steps, then K timed steps back to back between two HIP
-    events on the launch stream (synchronised on both sides);
-  * a second pass of K steps brackets only the split kernel with HIP events
-    (library measurement hook; same work) to give that kernel's average
-    duration, from which its achieved HBM bandwidth is computed on its
-    algorithmic bytes;
-  * the CPU oracle runs the same step on the host cores (one full step).
+  * W untimed warm-up steps, then 5 batches of K timed steps back to back,
+    each between two HIP events on the launch stream (synchronised on both
+    sides); the value is the median of the 5 batch means;
+  * 5 more batches of K steps bracket only the split kernel with HIP events
+    (library measurement hook; same work): the median batch mean is that
+    kernel's duration, from which its achieved HBM bandwidth is computed on
+    its algorithmic bytes (and its matrix-core rate on its products);
+  * the read ceiling of the same bytes (pdec_read_probe, plain reads and the
+    split pass's LDS-DMA ring with no arithmetic) is timed the same way;
+  * the CPU oracle runs the same step on the host cores (one full step), and
+    a sample of rows on one thread.
 
 Prints one JSON line.
 """
@@ -36,6 +40,8 @@ sys.path.insert(0, ROOT)
 METRIC = "µs/decode step + achieved HBM GB/s (% of peak) at prefix 32k, E=32 events"
 HBM_PEAK_GBPS = 8000.0
 ROTATE_BYTES = 512 << 20
+MFMA_PEAK_TFLOPS = 2500.0   # dense bf16 matrix-core peak
+BATCHES = 5
 
 
 def _log(*a):
@@ -68,7 +74,44 @@ def split_kernel_bytes(s) -> int:
     return 2 * int(s.cu_prefix[-1]) * row + 2 * int(s.event_lens.sum()) * row + s.num_events * s.H_q * s.D * b
 
 
+def split_kernel_flops(s) -> int:
+    """Matrix products of the split pass: every live (stream, head) row
+    against each key it sees (prefix and own rows), scores and P V, 2 flops
+    per multiply-add: 4 D per (row, key)."""
+    live = s.event_lens > 0
+    keys = 0
+    for v in range(s.num_videos):
+        e0, e1 = int(s.cu_events[v]), int(s.cu_events[v + 1])
+        L = int(s.cu_prefix[v + 1] - s.cu_prefix[v])
+        keys += int(live[e0:e1].sum()) * L + int(s.event_lens[e0:e1][live[e0:e1]].sum())
+    return 4 * s.D * s.H_q * keys
+
+
 PROFILE = os.path.join(ROOT, "profiles", "split_finish__long_L32768_E32__hbm_counters.txt")
+SQ_PROFILE = os.path.join(ROOT, "profiles", "split__long_L32768_E32__sq_counters.txt")
+
+
+def _profile_fields(path):
+    fields = {}
+    with open(path) as fh:
+        for line in fh:
+            if not line.startswith("#") and ":" in line:
+                k, v = line.split(":", 1)
+                fields[k.strip()] = v.strip()
+    return fields
+
+
+def measured_mfma_busy(workload_name: str, plan_mask: str, tiles: str):
+    """Fraction of SIMD cycles the matrix cores were busy during the split
+    kernel, from the stored SQ counters; None unless they were taken on this
+    workload with the kernels as built now."""
+    from paper_2607_02963_amd import _build
+    if workload_name != "long_L32768_E32" or plan_mask != "full" or tiles != "16" or not os.path.exists(SQ_PROFILE):
+        return None
+    fields = _profile_fields(SQ_PROFILE)
+    if fields.get("source_digest") != _build.source_digest():
+        return None
+    return float(fields["mfma_busy_frac"])
 
 
 def measured_traffic(workload_name: str, plan_mask: str):
@@ -89,8 +132,21 @@ def measured_traffic(workload_name: str, plan_mask: str):
     return int(fields["traffic_bytes_per_launch"])
 
 
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(s, plan):
-    """The oracle (as it stands) on the host cores: one full step, all rows."""
+    """The oracle (as it stands) on the host cores: one full step, all rows,
+    with every OpenMP thread; and a sample of rows on one thread, scaled to the
+    full step."""
     sys.path.insert(0, os.path.join(ROOT, "oracle"))
     import oracle
     threads = oracle.max_threads()
@@ -98,9 +154,71 @@ def cpu_baseline(s, plan):
     oracle.attn_step(s.q, s.k_prefix, s.v_prefix, s.k_event, s.v_event, s.event_lens, s.cu_prefix, s.cu_events,
                      scale=s.scale, threads=threads, **plan)
     dt = time.perf_counter() - t0
+    rows = s.num_events * s.H_q
+    nsel = min(rows, 64)
+    sel = np.linspace(0, rows - 1, nsel).astype(np.int64)
+    t0 = time.perf_counter()
+    oracle.attn_step(s.q, s.k_prefix, s.v_prefix, s.k_event, s.v_event, s.event_lens, s.cu_prefix, s.cu_events,
+                     scale=s.scale, threads=1, row_select=sel, **plan)
+    dt1 = (time.perf_counter() - t0) * rows / nsel
     return {"value": round(dt * 1e6, 1), "unit": "us/step", "cores": threads, "kind": "oracle",
-            "sample": f"one full step of {s.name}: all {s.num_events * s.H_q} (stream, head) rows, float64 "
-                      f"dense-mask oracle, OpenMP over rows"}
+            "sample": f"one full step of {s.name}: all {rows} (stream, head) rows, float64 "
+                      f"dense-mask oracle, OpenMP over rows",
+            "nproc": os.cpu_count(), "omp_max_threads": threads, "cpu_model": _cpu_model(),
+            "single_thread": {"value": round(dt1 * 1e6, 1), "unit": "us/step", "cores": 1,
+                              "sample": f"{nsel} of the {rows} rows on one thread, scaled to the full step"}}
+
+
+def _median_batches(run_batch):
+    """Median of BATCHES batch means (each batch returns its mean in ms)."""
+    vals = [run_batch(b) for b in range(BATCHES)]
+    return float(np.median(vals)), vals
+
+
+def read_ceiling(torch, pdec, nbytes: int, H_kv: int = 4, keys_per_item: int = 576, launches: int = 20):
+    """Time pdec_read_probe on a K/V pair of about nbytes ([L, H_kv, 128]
+    bf16 each), rotated over copies of >= 512 MB together, with HIP events
+    around each launch back to back (as the split kernel is timed)."""
+    L = max(64, int(round(nbytes / (2 * H_kv * 256) / 64)) * 64)
+    pair = 2 * L * H_kv * 256
+    ncopy = max(2, -(-ROTATE_BYTES // pair))
+    ks = [torch.ones(L, H_kv, 128, dtype=torch.bfloat16, device="cuda") for _ in range(ncopy)]
+    vs = [torch.ones(L, H_kv, 128, dtype=torch.bfloat16, device="cuda") for _ in range(ncopy)]
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+    res = {"bytes": pair, "L": L, "H_kv": H_kv}
+    for mode, name in ((0, "plain"), (1, "lds_ring")):
+        for i in range(4):
+            pdec.read_probe(ks[i % ncopy], vs[i % ncopy], mode, keys_per_item, sink, stream)
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(launches)]
+        for i in range(launches):
+            ev[i][0].record(stream)
+            pdec.read_probe(ks[i % ncopy], vs[i % ncopy], mode, keys_per_item, sink, stream)
+            ev[i][1].record(stream)
+        torch.cuda.synchronize()
+        us = float(np.median([a.elapsed_time(b) * 1e3 for a, b in ev]))
+        res[name + "_us"] = round(us, 3)
+        res[name + "_GBps"] = round(pair / (us * 1e-6) / 1e9, 1)
+    del ks, vs
+    torch.cuda.empty_cache()
+    return res
+
+
+def run_read_probe(args, torch, pdec):
+    """The read ceiling at 16, 32, 64 and 72 MB (decode-step K/V layout, 4 kv
+    heads): plain reads and the split pass's LDS-DMA ring, no arithmetic."""
+    rows = [read_ceiling(torch, pdec, mb << 20) for mb in (16, 32, 64, 72)]
+    for r in rows:
+        _log(f"bench: read probe {r['bytes'] / 1e6:.1f} MB: plain {r['plain_us']:.2f} us ({r['plain_GBps']:.0f} GB/s), "
+             f"LDS ring {r['lds_ring_us']:.2f} us ({r['lds_ring_GBps']:.0f} GB/s)")
+    head = rows[-1]
+    print(json.dumps({"metric": "streaming-read ceiling (GB/s) of a decode-step K/V pair in one launch",
+                      "value": head["plain_GBps"], "unit": "GB/s", "n_gpus": 1, "higher_is_better": True,
+                      "data": "synthetic", "dtype": "bf16",
+                      "config": {"workload": "read_probe", "sizes_MB": [16, 32, 64, 72], "H_kv": 4, "head_dim": 128},
+                      "roofline": {"bound": "hbm", "achieved": head["plain_GBps"], "peak": HBM_PEAK_GBPS,
+                                   "unit": "GB/s", "frac": round(head["plain_GBps"] / HBM_PEAK_GBPS, 4)},
+                      "results": rows}), flush=True)
 
 
 def run_loop(args, torch, pdec, wl):
@@ -523,7 +641,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="long_32k",
                     help="long_32k | single_8k | ragged_16 | tiny_f32 | loop_64 | rope_append | grounding | prefill"
-                         " | aggregation | prefix_causal | prefill_backward")
+                         " | aggregation | prefix_causal | prefill_backward | read_probe")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--plan-mask", choices=("full", "self"), default="full",
                     help="full: every stream sees all plan tokens (the full design); self: each stream sees only "
@@ -577,6 +695,9 @@ def main():
     if args.workload == "prefix_causal":
         run_prefix_causal(args, torch, pdec, wl)
         return
+    if args.workload == "read_probe":
+        run_read_probe(args, torch, pdec)
+        return
     if args.workload == "aggregation":
         run_aggregation(args, torch, pdec, wl)
         return
@@ -621,30 +742,44 @@ def main():
         step(i)
     torch.cuda.synchronize()
 
-    t0 = torch.cuda.Event(enable_timing=True)
-    t1 = torch.cuda.Event(enable_timing=True)
-    t0.record(stream)
-    for i in range(args.steps):
-        step(i)
-    t1.record(stream)
-    torch.cuda.synchronize()
-    ms = t0.elapsed_time(t1) / args.steps
-    _log(f"bench: timed {args.steps} steps: {ms * 1e3:.2f} us/step")
-
-    timer = pdec.SplitTimer(args.steps)
-    with timer:
+    def step_batch(b):
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record(stream)
         for i in range(args.steps):
-            step(i)
-    torch.cuda.synchronize()
-    kms = timer.durations_ms(args.steps)
-    timer.close()
-    split_ms = float(np.mean(kms))
-    _log(f"bench: split kernel {split_ms * 1e3:.2f} us avg (min {min(kms) * 1e3:.2f}, max {max(kms) * 1e3:.2f})")
+            step(b * args.steps + i)
+        t1.record(stream)
+        torch.cuda.synchronize()
+        return t0.elapsed_time(t1) / args.steps
+
+    ms, batch_ms = _median_batches(step_batch)
+    _log(f"bench: {BATCHES} batches of {args.steps} steps: " + " ".join(f"{x * 1e3:.2f}" for x in batch_ms) +
+         f" us/step (median {ms * 1e3:.2f})")
+
+    def split_batch(b):
+        timer = pdec.SplitTimer(args.steps)
+        with timer:
+            for i in range(args.steps):
+                step(b * args.steps + i)
+        torch.cuda.synchronize()
+        kms = timer.durations_ms(args.steps)
+        timer.close()
+        return float(np.mean(kms))
+
+    split_ms, split_batches = _median_batches(split_batch)
+    _log(f"bench: split kernel " + " ".join(f"{x * 1e3:.2f}" for x in split_batches) +
+         f" us (median of batch means {split_ms * 1e3:.2f})")
+    kbytes_ = split_kernel_bytes(s)
+    ceiling = read_ceiling(torch, pdec, kbytes_, H_kv=s.H_kv, keys_per_item=chunk) if s.D == 128 else None
+    if ceiling:
+        _log(f"bench: read ceiling of {ceiling['bytes'] / 1e6:.1f} MB: plain {ceiling['plain_us']:.2f} us, "
+             f"LDS ring {ceiling['lds_ring_us']:.2f} us")
 
     alg = s.algorithmic_bytes()
     gbps = alg / (ms * 1e-3) / 1e9
-    kbytes = split_kernel_bytes(s)
+    kbytes = kbytes_
     kgbps = kbytes / (split_ms * 1e-3) / 1e9
+    kflops = split_kernel_flops(s)
     live = int((s.event_lens > 0).sum())
     rec = {
         "metric": METRIC,
@@ -670,8 +805,18 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(kgbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(kgbps / HBM_PEAK_GBPS, 4), "traffic": measured_traffic(s.name, args.plan_mask),
                      "kernel": "split pass (shared prefix + stream rows)", "kernel_us": round(split_ms * 1e3, 3),
-                     "kernel_algorithmic_bytes": kbytes},
+                     "kernel_us_source": "HIP events around each split launch, back to back on the launch stream; "
+                                         f"median of {BATCHES} batch means of {args.steps} launches",
+                     "kernel_algorithmic_bytes": kbytes,
+                     "mfma_util": round(kflops / (split_ms * 1e-3) / 1e12 / MFMA_PEAK_TFLOPS, 4),
+                     "mfma_tflops": round(kflops / (split_ms * 1e-3) / 1e12, 1),
+                     "mfma_busy_frac": measured_mfma_busy(s.name, args.plan_mask, args.tiles)},
+        "batch_us_per_step": [round(x * 1e3, 3) for x in batch_ms],
     }
+    if ceiling:
+        rec["read_ceiling"] = ceiling
+        rec["roofline"]["frac_of_read_ceiling"] = round(kgbps / ceiling["plain_GBps"], 4)
+        rec["roofline"]["frac_of_ring_ceiling"] = round(kgbps / ceiling["lds_ring_GBps"], 4)
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(s, plan)
     print(json.dumps(rec), flush=True)

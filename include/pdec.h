@@ -38,6 +38,11 @@
  *    memory are a caller contract (0 <= n_e <= event_cap, 0 <= prefix length
  *    <= max_prefix_len, non-decreasing offsets); they are not checked.
  *  - Calls sharing one workspace must not overlap in time.
+ *  - Debug mode: with the environment variable PDEC_DEBUG=1 (read once, when
+ *    the library is first used), the step calls copy the device lengths to the
+ *    host (synchronising `stream`), check them with pdec_check_lengths, and
+ *    return PDEC_ERR_BAD_LENGTHS before launching anything if they break the
+ *    contract.  Off by default: a step then never synchronises.
  */
 #ifndef PDEC_H
 #define PDEC_H
@@ -55,6 +60,8 @@ typedef enum {
     PDEC_ERR_UNSUPPORTED = -2, /* a size or type this build has no kernel for (D, dtype) */
     PDEC_ERR_WORKSPACE = -3,   /* workspace smaller than pdec_workspace_size()          */
     PDEC_ERR_HIP = -4,         /* a HIP runtime call or kernel launch failed             */
+    PDEC_ERR_BAD_LENGTHS = -5, /* a length held in device memory breaks the contract     */
+                               /* (only detected with PDEC_DEBUG=1, see below)           */
     PDEC_ERR_SCRATCH = -6      /* the step needs more scratch than the library's static  */
                                /* buffer holds (pdec_attn_step_noalloc only)             */
 } pdec_status;
@@ -262,9 +269,45 @@ int pdec_describe_plan(const pdec_dims* dims, int32_t num_videos, pdec_plan_info
  * hipEventRecord(stop_events[i % n]) on the call's stream, so a caller can
  * time that kernel alone without changing the work done.  The events are
  * hipEvent_t handles owned by the caller.  n = 0 (or NULL arrays) turns the
- * hook off.  Process-wide, not thread-safe.  Returns a pdec_status.
+ * hook off.  Process-wide; the hook's state is guarded by a lock, so step
+ * calls from several threads each take their own event pair (in call order).
+ * Returns a pdec_status.
  */
 int pdec_set_split_timer(void* const* start_events, void* const* stop_events, int n);
+
+/*
+ * The device-length contract, checked on HOST copies of the length arrays
+ * (the check PDEC_DEBUG=1 runs before a step): 0 <= event_lens[e] <=
+ * event_cap for every stream; with num_videos == 1, prefix_lens[0] in
+ * [0, max_prefix_len]; with num_videos > 1, cu_prefix and cu_events start at
+ * 0, never decrease, end at the total prefix rows (when dims->prefix_tokens
+ * > 0) and at num_events, and each video's prefix (cu_prefix[v+1] -
+ * cu_prefix[v]) is at most max_prefix_len and its stream count at most
+ * max_events_per_video (when > 0).  Pass prefix_lens for one video, or
+ * cu_prefix and cu_events for a ragged batch.  Returns PDEC_OK,
+ * PDEC_ERR_BAD_LENGTHS, or PDEC_ERR_INVALID_ARG for invalid dims or missing
+ * arrays.  Host-only; reads num_events + num_videos + 1 values at most.
+ */
+int pdec_check_lengths(const pdec_dims* dims, int32_t num_videos, const int32_t* event_lens,
+                       const int32_t* prefix_lens, const int32_t* cu_prefix, const int32_t* cu_events);
+
+/*
+ * Measurement aid (the read ceiling the split pass is compared with): streams
+ * a K/V cache pair of the decode step's layout, k and v each [L, H_kv, 128]
+ * bfloat16 in device memory (16-byte aligned), once, computing nothing.
+ *   mode 0: plain 16-byte loads, each work-group a contiguous slab (the
+ *           HBM read ceiling for these bytes in one launch);
+ *   mode 1: the split pass's memory path: items of (kv head, keys_per_item
+ *           keys, a multiple of 64), every 64-key stage of the head's key and
+ *           value rows moved into a 4-stage LDS ring by direct-to-LDS loads
+ *           with a work-group barrier per stage.
+ * sink: device int32, written only when the data hash to a fixed value (so
+ * the reads cannot be optimised away).  Asynchronous on `stream`.  Returns
+ * PDEC_ERR_INVALID_ARG for null or misaligned pointers, L or H_kv < 1, a mode
+ * other than 0 or 1, or (mode 1) keys_per_item not a positive multiple of 64.
+ */
+int pdec_read_probe(const void* k, const void* v, int32_t L, int32_t H_kv, int32_t keys_per_item, int32_t mode,
+                    int32_t* sink, void* stream);
 
 /*
  * Segment-level similarity grounding at inference (App. "More Implementation

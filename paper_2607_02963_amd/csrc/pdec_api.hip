@@ -18,6 +18,7 @@
 #include <cstdlib>
 #include <mutex>
 #include <type_traits>
+#include <vector>
 
 #include "pdec.h"
 
@@ -62,11 +63,35 @@ void* scratch_address()
     return g_scratch_ptr[dev];
 }
 
-// measurement hook (pdec_set_split_timer)
+// measurement hook (pdec_set_split_timer), guarded by g_timer_mutex
+std::mutex g_timer_mutex;
 void* const* g_timer_start = nullptr;
 void* const* g_timer_stop = nullptr;
 int g_timer_n = 0;
 long g_timer_calls = 0;
+std::atomic<bool> g_timer_on{false};
+
+// The split-kernel events of this call (both null when the hook is off).
+void timer_slot_events(hipEvent_t* start, hipEvent_t* stop)
+{
+    *start = *stop = nullptr;
+    if (!g_timer_on.load(std::memory_order_acquire)) return;
+    std::lock_guard<std::mutex> lock(g_timer_mutex);
+    if (g_timer_n <= 0) return;
+    const int slot = (int)(g_timer_calls++ % g_timer_n);
+    *start = static_cast<hipEvent_t>(g_timer_start[slot]);
+    *stop = static_cast<hipEvent_t>(g_timer_stop[slot]);
+}
+
+// Debug mode (PDEC_DEBUG=1): device lengths are checked before each step.
+bool debug_mode()
+{
+    static const bool on = [] {
+        const char* v = std::getenv("PDEC_DEBUG");
+        return v && v[0] == '1' && v[1] == '\0';
+    }();
+    return on;
+}
 
 struct Plan {
     int path;
@@ -209,6 +234,48 @@ void launch_valu(const StepArgs& a, int grid, hipStream_t s)
     else launch_valu_kernel<T, D, false>(a, grid, s);
 }
 
+// The device-length contract on host copies (pdec_check_lengths).
+int check_lengths(const pdec_dims* d, int num_videos, const int32_t* event_lens, const int32_t* prefix_lens,
+                  const int32_t* cu_prefix, const int32_t* cu_events)
+{
+    if (!event_lens) return PDEC_ERR_INVALID_ARG;
+    for (int e = 0; e < d->num_events; ++e)
+        if (event_lens[e] < 0 || event_lens[e] > d->event_cap) return PDEC_ERR_BAD_LENGTHS;
+    if (num_videos == 1 && !cu_prefix) {
+        if (!prefix_lens) return PDEC_ERR_INVALID_ARG;
+        return prefix_lens[0] < 0 || prefix_lens[0] > d->max_prefix_len ? PDEC_ERR_BAD_LENGTHS : PDEC_OK;
+    }
+    if (!cu_prefix || !cu_events) return PDEC_ERR_INVALID_ARG;
+    if (cu_prefix[0] != 0 || cu_events[0] != 0 || cu_events[num_videos] != d->num_events) return PDEC_ERR_BAD_LENGTHS;
+    if (d->prefix_tokens > 0 && cu_prefix[num_videos] != d->prefix_tokens) return PDEC_ERR_BAD_LENGTHS;
+    const int ev = events_per_video(d);
+    for (int v = 0; v < num_videos; ++v) {
+        const long L = (long)cu_prefix[v + 1] - cu_prefix[v], E = (long)cu_events[v + 1] - cu_events[v];
+        if (L < 0 || L > d->max_prefix_len || E < 0 || E > ev) return PDEC_ERR_BAD_LENGTHS;
+    }
+    return PDEC_OK;
+}
+
+// PDEC_DEBUG=1: copies the device lengths to the host (synchronising the
+// stream) and checks them.
+int debug_check_lengths(const pdec_dims* d, int num_videos, const int32_t* event_lens, const int32_t* prefix_len,
+                        const int32_t* cu_prefix, const int32_t* cu_events, hipStream_t s)
+{
+    std::vector<int32_t> ev(d->num_events), pl(1), cp(num_videos + 1), ce(num_videos + 1);
+    if (hipMemcpyAsync(ev.data(), event_lens, ev.size() * 4, hipMemcpyDeviceToHost, s) != hipSuccess)
+        return PDEC_ERR_HIP;
+    if (cu_prefix) {
+        if (hipMemcpyAsync(cp.data(), cu_prefix, cp.size() * 4, hipMemcpyDeviceToHost, s) != hipSuccess ||
+            hipMemcpyAsync(ce.data(), cu_events, ce.size() * 4, hipMemcpyDeviceToHost, s) != hipSuccess)
+            return PDEC_ERR_HIP;
+    } else if (hipMemcpyAsync(pl.data(), prefix_len, 4, hipMemcpyDeviceToHost, s) != hipSuccess) {
+        return PDEC_ERR_HIP;
+    }
+    if (hipStreamSynchronize(s) != hipSuccess) return PDEC_ERR_HIP;
+    return check_lengths(d, num_videos, ev.data(), pl.data(), cu_prefix ? cp.data() : nullptr,
+                         cu_prefix ? ce.data() : nullptr);
+}
+
 int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_prefix, const void* v_prefix,
              const int32_t* cu_prefix, const int32_t* prefix_len, const void* k_event, const void* v_event,
              const int32_t* event_lens, const int32_t* cu_events, void* out, float* lse, void* workspace,
@@ -232,6 +299,10 @@ int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_pr
     const Plan p = make_plan(d, num_videos);
     if (workspace_bytes < p.ws_bytes) return PDEC_ERR_WORKSPACE;
     if (8 * ceil_div(p.n_items, 8) > (long)INT32_MAX) return PDEC_ERR_UNSUPPORTED;
+    if (debug_mode() &&
+        (rc = debug_check_lengths(d, num_videos, event_lens, prefix_len, cu_prefix, cu_events,
+                                  static_cast<hipStream_t>(stream))) != PDEC_OK)
+        return rc;
 
     StepArgs a{};
     a.q = q;
@@ -272,9 +343,9 @@ int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_pr
     hipStream_t s = static_cast<hipStream_t>(stream);
     const int grid = 8 * a.items_per_xcd;
     const bool bf16 = d->dtype == PDEC_DTYPE_BF16;
-    const int timer_slot = g_timer_n > 0 ? (int)(g_timer_calls++ % g_timer_n) : -1;
-    if (timer_slot >= 0 && hipEventRecord(static_cast<hipEvent_t>(g_timer_start[timer_slot]), s) != hipSuccess)
-        return PDEC_ERR_HIP;
+    hipEvent_t ev_start, ev_stop;
+    timer_slot_events(&ev_start, &ev_stop);
+    if (ev_start && hipEventRecord(ev_start, s) != hipSuccess) return PDEC_ERR_HIP;
     if (p.path == kPathMfma) {
         launch_split_mfma(a, p.shape, grid, s);
     } else if (bf16) {
@@ -285,8 +356,7 @@ int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_pr
         else launch_valu<float, 64>(a, grid, s);
     }
     if ((rc = launch_status()) != PDEC_OK) return rc;
-    if (timer_slot >= 0 && hipEventRecord(static_cast<hipEvent_t>(g_timer_stop[timer_slot]), s) != hipSuccess)
-        return PDEC_ERR_HIP;
+    if (ev_stop && hipEventRecord(ev_stop, s) != hipSuccess) return PDEC_ERR_HIP;
     // one chunk per row on the matrix-core path: the split pass wrote the result
     if (p.path == kPathMfma && p.max_chunks == 1) return PDEC_OK;
     const int fgrid = (int)rows;
@@ -313,6 +383,7 @@ const char* pdec_strerror(int status)
     case PDEC_ERR_UNSUPPORTED: return "unsupported size or type (head_dim must be 64 or 128, dtype f32 or bf16)";
     case PDEC_ERR_WORKSPACE: return "workspace smaller than pdec_workspace_size()";
     case PDEC_ERR_HIP: return "HIP runtime error or kernel launch failure";
+    case PDEC_ERR_BAD_LENGTHS: return "a length held in device memory breaks the contract (PDEC_DEBUG=1 check)";
     case PDEC_ERR_SCRATCH: return "step needs more scratch than the static buffer of pdec_attn_step_noalloc holds";
     default: return "unknown pdec status";
     }
@@ -437,11 +508,21 @@ int pdec_set_split_timer(void* const* start_events, void* const* stop_events, in
 {
     if (n < 0) return PDEC_ERR_INVALID_ARG;
     if (n > 0 && (!start_events || !stop_events)) return PDEC_ERR_INVALID_ARG;
+    std::lock_guard<std::mutex> lock(g_timer_mutex);
     g_timer_start = n > 0 ? start_events : nullptr;
     g_timer_stop = n > 0 ? stop_events : nullptr;
     g_timer_n = n;
     g_timer_calls = 0;
+    g_timer_on.store(n > 0, std::memory_order_release);
     return PDEC_OK;
+}
+
+int pdec_check_lengths(const pdec_dims* dims, int32_t num_videos, const int32_t* event_lens,
+                       const int32_t* prefix_lens, const int32_t* cu_prefix, const int32_t* cu_events)
+{
+    const int rc = validate_dims(dims, num_videos);
+    if (rc != PDEC_OK) return rc;
+    return check_lengths(dims, num_videos, event_lens, prefix_lens, cu_prefix, cu_events);
 }
 
 int pdec_query_plan(const pdec_dims* dims, int32_t num_videos, int32_t* path, int32_t* chunk_keys)

@@ -20,6 +20,7 @@ PDEC_ERR_INVALID_ARG = -1
 PDEC_ERR_UNSUPPORTED = -2
 PDEC_ERR_WORKSPACE = -3
 PDEC_ERR_HIP = -4
+PDEC_ERR_BAD_LENGTHS = -5
 PDEC_ERR_SCRATCH = -6
 NOALLOC_SCRATCH_BYTES = 32 << 20
 PDEC_DTYPE_F32 = 0
@@ -31,7 +32,7 @@ EXPORTED = ("pdec_strerror", "pdec_workspace_size", "pdec_attn_step", "pdec_attn
             "pdec_kv_append", "pdec_rope_kv_append", "pdec_set_path", "pdec_query_plan",
             "pdec_set_split_timer", "pdec_describe_plan", "pdec_grounding_workspace_size", "pdec_segment_grounding",
             "pdec_aggregation_workspace_size", "pdec_aggregate", "pdec_backward_workspace_size",
-            "pdec_attn_prefill_backward")
+            "pdec_attn_prefill_backward", "pdec_read_probe", "pdec_check_lengths")
 
 AGGR_MODES = {"uniform": 0, "learned": 1, "attention": 2}
 
@@ -131,6 +132,12 @@ def lib():
         L.pdec_describe_plan.argtypes = [dp, i32, ctypes.POINTER(PlanInfo)]
         L.pdec_set_split_timer.restype = ctypes.c_int
         L.pdec_set_split_timer.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int]
+        L.pdec_check_lengths.restype = ctypes.c_int
+        L.pdec_check_lengths.argtypes = [dp, i32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                         ctypes.c_void_p]
+        L.pdec_read_probe.restype = ctypes.c_int
+        L.pdec_read_probe.argtypes = [ctypes.c_void_p, ctypes.c_void_p, i32, i32, i32, i32, ctypes.c_void_p,
+                                      ctypes.c_void_p]
         _lib = L
     return _lib
 
@@ -548,6 +555,35 @@ def aggregate(g, x, cu_seg, salient, mode, *, scores=None, q=None, k=None, lse=N
             ctypes.c_size_t(workspace.numel() * workspace.element_size()), _stream(stream, g.device)]
     _check("pdec_aggregate", lib().pdec_aggregate(ctypes.byref(dims), *args))
     return out
+
+
+def check_lengths(dims: Dims, num_videos: int, event_lens, prefix_lens=None, cu_prefix=None, cu_events=None) -> int:
+    """pdec_check_lengths on host int32 arrays (numpy or lists); returns the
+    status code (PDEC_OK or PDEC_ERR_BAD_LENGTHS), raising only for invalid
+    dims or missing arrays."""
+    import numpy as np
+    arrs = [None if x is None else np.ascontiguousarray(np.asarray(x, dtype=np.int32))
+            for x in (event_lens, prefix_lens, cu_prefix, cu_events)]
+    ptrs = [None if x is None else x.ctypes.data for x in arrs]
+    rc = lib().pdec_check_lengths(ctypes.byref(dims), num_videos, *ptrs)
+    if rc not in (PDEC_OK, PDEC_ERR_BAD_LENGTHS):
+        raise PdecError("pdec_check_lengths", rc)
+    return rc
+
+
+def read_probe(k, v, mode: int, keys_per_item: int = 576, sink=None, stream=None):
+    """pdec_read_probe: stream the K/V pair k, v ([L, H_kv, 128] bf16 on the
+    device) once; mode 0 plain reads, mode 1 the split pass's LDS-DMA ring."""
+    for t in (k, v):
+        if t.dtype != torch.bfloat16 or not t.is_cuda or t.dim() != 3 or t.shape[2] != 128 or not t.is_contiguous():
+            raise ValueError("k and v must be contiguous [L, H_kv, 128] bfloat16 device tensors")
+    if k.shape != v.shape:
+        raise ValueError("k and v must have one shape")
+    if sink is None:
+        sink = torch.zeros(1, dtype=torch.int32, device=k.device)
+    _check("pdec_read_probe", lib().pdec_read_probe(k.data_ptr(), v.data_ptr(), k.shape[0], k.shape[1],
+                                                    keys_per_item, mode, sink.data_ptr(), _stream(stream, k.device)))
+    return sink
 
 
 class SplitTimer:

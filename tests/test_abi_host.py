@@ -219,3 +219,38 @@ def test_describe_plan_matches_query_plan_and_shapes():
     with pytest.raises(pdec.PdecError):
         pdec.describe_plan(_dims(H_q=27))
     assert pdec.lib().pdec_describe_plan(ctypes.byref(_dims()), 1, None) == pdec.PDEC_ERR_INVALID_ARG
+
+
+def test_length_contract_check_on_host_arrays():
+    """pdec_check_lengths (the PDEC_DEBUG=1 check) on host copies: each broken
+    clause of the device-length contract is caught, valid lengths pass."""
+    d = _dims(num_events=4, cap=10, max_prefix_len=100)
+    ok = pdec.PDEC_OK
+    bad = pdec.PDEC_ERR_BAD_LENGTHS
+    assert pdec.check_lengths(d, 1, [1, 10, 0, 3], prefix_lens=[100]) == ok
+    assert pdec.check_lengths(d, 1, [1, 11, 0, 3], prefix_lens=[100]) == bad      # n_e > cap
+    assert pdec.check_lengths(d, 1, [1, -1, 0, 3], prefix_lens=[100]) == bad      # n_e < 0
+    assert pdec.check_lengths(d, 1, [1, 2, 0, 3], prefix_lens=[101]) == bad       # L > max_prefix_len
+    assert pdec.check_lengths(d, 1, [1, 2, 0, 3], prefix_lens=[-1]) == bad
+    dr = pdec.make_dims(4, 28, 4, 128, 10, 100, pdec.PDEC_DTYPE_BF16, max_events_per_video=3, prefix_tokens=150)
+    assert pdec.check_lengths(dr, 2, [1, 2, 3, 4], cu_prefix=[0, 100, 150], cu_events=[0, 3, 4]) == ok
+    assert pdec.check_lengths(dr, 2, [1, 2, 3, 4], cu_prefix=[0, 101, 150], cu_events=[0, 3, 4]) == bad  # L_v > max
+    assert pdec.check_lengths(dr, 2, [1, 2, 3, 4], cu_prefix=[0, 100, 149], cu_events=[0, 3, 4]) == bad  # != tokens
+    assert pdec.check_lengths(dr, 2, [1, 2, 3, 4], cu_prefix=[1, 100, 150], cu_events=[0, 3, 4]) == bad  # not from 0
+    assert pdec.check_lengths(dr, 2, [1, 2, 3, 4], cu_prefix=[0, 100, 150], cu_events=[0, 4, 4]) == bad  # E_v > max
+    assert pdec.check_lengths(dr, 2, [1, 2, 3, 4], cu_prefix=[0, 100, 150], cu_events=[0, 3, 3]) == bad  # != E
+    assert pdec.check_lengths(dr, 2, [1, 2, 3, 4], cu_prefix=[0, 100, 150], cu_events=[0, 2, 1]) == bad  # decreasing
+    with pytest.raises(pdec.PdecError):
+        pdec.check_lengths(dr, 2, [1, 2, 3, 4], cu_prefix=[0, 100, 150])             # cu_events missing
+    assert pdec.lib().pdec_strerror(pdec.PDEC_ERR_BAD_LENGTHS).decode().startswith("a length held")
+
+
+def test_read_probe_rejects_bad_arguments_before_launch():
+    """pdec_read_probe refuses invalid arguments on the host (no GPU needed)."""
+    L = pdec.lib()
+    fake = 1 << 20  # aligned, never dereferenced: every call below is refused before any launch
+    assert L.pdec_read_probe(None, fake, 64, 4, 576, 0, fake, None) == pdec.PDEC_ERR_INVALID_ARG
+    assert L.pdec_read_probe(fake + 8, fake, 64, 4, 576, 0, fake, None) == pdec.PDEC_ERR_INVALID_ARG
+    assert L.pdec_read_probe(fake, fake, 0, 4, 576, 0, fake, None) == pdec.PDEC_ERR_INVALID_ARG
+    assert L.pdec_read_probe(fake, fake, 64, 4, 576, 2, fake, None) == pdec.PDEC_ERR_INVALID_ARG
+    assert L.pdec_read_probe(fake, fake, 64, 4, 100, 1, fake, None) == pdec.PDEC_ERR_INVALID_ARG
