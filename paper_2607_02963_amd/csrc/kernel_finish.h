@@ -12,135 +12,116 @@
 // l = 0, u = 0 and a reference m far below any score, so its weight is 0.
 // A stream with n_e == 0 has ended: out row 0, lse -inf.
 //
-// One work-group of four waves per row.  A row's slots are contiguous in the
-// workspace ([row][slot][D] and [row][slot](m, l)).  The lanes form 4*SG
-// slot groups of D/4 lanes (4 d each); group s takes slots s, s + 4SG, ...
-// Their first NL slots are loaded before anything else (slot indices clamped
-// to the last slot, so the loads need no branch and the compiler issues them
-// together), so those loads are in flight while wave 0 reduces (M, L) and
-// stores the slot weights
-// 2^(m_c - M) l_c in LDS; the group sums then meet through lane shuffles and LDS.
+// One wave per row, four rows per work-group.  The D elements of a slot are
+// read by LPS lanes with 16-byte loads, SPI slots per wave instruction; lane
+// group j (lanes j*LPS ..) takes slots j, j + SPI, ... of a batch of SPI*NB
+// slots, and every load of a batch (partial outputs and (m, l) pairs, slot
+// indices clamped to the last slot so no load needs a branch) is issued
+// before any arithmetic, so a row costs one memory round trip.  The batch
+// maximum is formed over the lane groups by lane exchanges, so every lane
+// weighs its slots with the same M; the weighted sums then meet the same way.
+// Rows with more slots than one batch fold batches in with a rescale.
 #pragma once
 
 #include "pdec_common.h"
 
 namespace pdec {
 
-constexpr int kMaxChunks = 512;  // slot weights held in LDS per row
-
-// Four consecutive partial-output elements as floats.
-__device__ inline float4 load_part4(const float* p) { return *reinterpret_cast<const float4*>(p); }
-__device__ inline float4 load_part4(const uint16_t* p)
-{
-    const uint2 u = *reinterpret_cast<const uint2*>(p);
-    return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u), __uint_as_float(u.y << 16),
-                       __uint_as_float(u.y & 0xffff0000u));
-}
+constexpr int kMaxChunks = 512;  // largest slot count per row the host plans
 
 template <typename T, int D>
 __global__ __launch_bounds__(256) void finish_kernel(StepArgs a)
 {
-    constexpr int NW = 4;             // waves per row
-    constexpr int TPR = D / 4;        // lanes per slot group
-    constexpr int SG = 64 / TPR;      // slot groups per wave
-    constexpr int GS = NW * SG;       // slot groups per row
-    constexpr int NL = 64 / GS;       // slots per group loaded up front (64 slots in all)
-    static_assert(SG * TPR == 64, "head_dim 64 or 128");
-    __shared__ float wts[kMaxChunks];
-    __shared__ float4 red[NW][TPR];
-    __shared__ float ML_s[2];
+    constexpr int EPL = 16 / (int)sizeof(T);  // elements per lane and slot
+    constexpr int LPS = D / EPL;              // lanes per slot
+    constexpr int SPI = 64 / LPS;             // slots per wave instruction
+    constexpr int NB = 64 / SPI < 16 ? 64 / SPI : 16;  // slots per lane and batch
+    constexpr int BATCH = SPI * NB;
+    static_assert(LPS * EPL == D && SPI * LPS == 64, "head_dim 64 or 128");
+    typedef __attribute__((ext_vector_type(4))) uint32_t u32x4_t;
 
-    const int tid = threadIdx.x;
-    const int wave = tid >> 6;
-    const int lane = tid & 63;
-    const long qr = blockIdx.x;  // (stream, head) row
+    const int wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    const long rows = (long)a.num_events * a.H_q * a.qps;
+    const long qr = (long)blockIdx.x * 4 + wave;  // (stream, head) row
+    if (qr >= rows) return;
     const int e = (int)(qr / ((long)a.H_q * a.qps));
-    T* __restrict__ out = static_cast<T*>(a.out) + qr * D;
+    const int j = lane / LPS;
+    const int d0 = EPL * (lane % LPS);
+    T* __restrict__ out = static_cast<T*>(a.out) + qr * D + d0;
 
-    if (a.event_lens[e] <= 0) {  // ended stream: uniform over the work-group
-        if (tid < D) out[tid] = from_f32<T>(0.f);
-        if (a.lse && tid == 0) a.lse[qr] = kNegInf;
+    if (a.event_lens[e] <= 0) {  // ended stream: uniform over the wave
+        if (j == 0) *reinterpret_cast<u32x4_t*>(out) = u32x4_t{0u, 0u, 0u, 0u};
+        if (a.lse && lane == 0) a.lse[qr] = kNegInf;
         return;
     }
     const int nch = min(a.video_chunks[video_of_event(a, e)], a.max_chunks);
-    const int grp = wave * SG + lane / TPR;
-    const int d0 = 4 * (lane % TPR);
     const T* __restrict__ po = static_cast<const T*>(a.part_o) + qr * a.max_chunks * D + d0;
+    const float2* __restrict__ pml = reinterpret_cast<const float2*>(a.part_ml) + qr * a.max_chunks;
 
-    float4 x[NL];
+    float M = -1e30f;  // finite: the first rescale multiplies zeros by 2^(-huge) = 0
+    float lsum = 0.f;
+    float acc[EPL];
 #pragma unroll
-    for (int i = 0; i < NL; ++i) {
-        const int c = grp + GS * i;
-        x[i] = load_part4(po + (long)min(c, nch - 1) * D);  // unconditional: all loads in flight at once
-    }
-
-    if (wave == 0) {
-        const float2* __restrict__ ml = reinterpret_cast<const float2*>(a.part_ml) + qr * a.max_chunks;
-        float mx = kNegInf;
-        for (int c = lane; c < nch; c += 64) mx = fmaxf(mx, ml[c].x);
+    for (int k = 0; k < EPL; ++k) acc[k] = 0.f;
+    for (int c0 = 0; c0 < nch; c0 += BATCH) {
+        u32x4_t x[NB];
+        float2 ml[NB];
 #pragma unroll
-        for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
-        float ls = 0.f;
-        for (int c = lane; c < nch; c += 64) {
-            const float2 s = ml[c];
-            const float w = fast_exp2(s.x - mx) * s.y;  // 0 for a slot without keys of this row
-            wts[c] = w;
-            ls += w;
+        for (int i = 0; i < NB; ++i) {
+            const int c = min(c0 + j + SPI * i, nch - 1);
+            x[i] = *reinterpret_cast<const u32x4_t*>(po + (long)c * D);
+            ml[i] = pml[c];
         }
+        float mb = M;
 #pragma unroll
-        for (int off = 32; off > 0; off >>= 1) ls += __shfl_xor(ls, off);
-        if (lane == 0) {
-            ML_s[0] = mx;
-            ML_s[1] = ls;
+        for (int i = 0; i < NB; ++i)
+            if (c0 + j + SPI * i < nch) mb = fmaxf(mb, ml[i].x);
+#pragma unroll
+        for (int off = LPS; off < 64; off <<= 1) mb = fmaxf(mb, __shfl_xor(mb, off));
+        const float r = fast_exp2(M - mb);
+        M = mb;
+        lsum *= r;
+#pragma unroll
+        for (int k = 0; k < EPL; ++k) acc[k] *= r;
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+            // 0 for a slot past the row's last, and for one without keys of the row
+            const float w = c0 + j + SPI * i < nch ? fast_exp2(ml[i].x - M) * ml[i].y : 0.f;
+            lsum += w;
+            if constexpr (sizeof(T) == 2) {
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    acc[2 * k] += w * __uint_as_float(x[i][k] << 16);
+                    acc[2 * k + 1] += w * __uint_as_float(x[i][k] & 0xffff0000u);
+                }
+            } else {
+#pragma unroll
+                for (int k = 0; k < 4; ++k) acc[k] += w * __uint_as_float(x[i][k]);
+            }
         }
     }
-    __syncthreads();
-
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-    for (int i = 0; i < NL; ++i) {
-        const int c = grp + GS * i;
-        if (c < nch) {
-            const float w = wts[c];
-            acc.x += w * x[i].x;
-            acc.y += w * x[i].y;
-            acc.z += w * x[i].z;
-            acc.w += w * x[i].w;
+    for (int off = LPS; off < 64; off <<= 1) {
+        lsum += __shfl_xor(lsum, off);
+#pragma unroll
+        for (int k = 0; k < EPL; ++k) acc[k] += __shfl_xor(acc[k], off);
+    }
+    if (j == 0) {
+        const float inv = 1.f / lsum;
+        if constexpr (sizeof(T) == 2) {
+            u32x4_t y;
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+                y[k] = (uint32_t)from_f32<uint16_t>(acc[2 * k] * inv) | ((uint32_t)from_f32<uint16_t>(acc[2 * k + 1] * inv) << 16);
+            *reinterpret_cast<u32x4_t*>(out) = y;
+        } else {
+            u32x4_t y;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) y[k] = __float_as_uint(acc[k] * inv);
+            *reinterpret_cast<u32x4_t*>(out) = y;
         }
-    }
-    for (int c = grp + GS * NL; c < nch; c += GS) {  // rows with more than 64 slots
-        const float w = wts[c];
-        const float4 y = load_part4(po + (long)c * D);
-        acc.x += w * y.x;
-        acc.y += w * y.y;
-        acc.z += w * y.z;
-        acc.w += w * y.w;
-    }
-#pragma unroll
-    for (int off = TPR; off < 64; off <<= 1) {
-        acc.x += __shfl_xor(acc.x, off);
-        acc.y += __shfl_xor(acc.y, off);
-        acc.z += __shfl_xor(acc.z, off);
-        acc.w += __shfl_xor(acc.w, off);
-    }
-    if (lane < TPR) red[wave][lane] = acc;
-    __syncthreads();
-    if (wave == 0 && lane < TPR) {
-#pragma unroll
-        for (int w = 1; w < NW; ++w) {
-            const float4 y = red[w][lane];
-            acc.x += y.x;
-            acc.y += y.y;
-            acc.z += y.z;
-            acc.w += y.w;
-        }
-        const float mx = ML_s[0], ls = ML_s[1];
-        const float inv = 1.f / ls;
-        out[d0] = from_f32<T>(acc.x * inv);
-        out[d0 + 1] = from_f32<T>(acc.y * inv);
-        out[d0 + 2] = from_f32<T>(acc.z * inv);
-        out[d0 + 3] = from_f32<T>(acc.w * inv);
-        if (a.lse && lane == 0) a.lse[qr] = kLn2 * (mx + __log2f(ls));
+        if (a.lse && lane == 0) a.lse[qr] = kLn2 * (M + __log2f(lsum));
     }
 }
 

@@ -183,6 +183,39 @@ __global__ __launch_bounds__(64 * WR * WK) void split_mfma_kernel(StepArgs a)
     const uint16_t* __restrict__ vev = static_cast<const uint16_t*>(a.v_event);
     const long stride = (long)a.H_kv * D;
 
+    // DMA of one stage (unit u0 + st): this wave's DMA_PER_WAVE 1 KB pieces,
+    // all of K or all of V.  Piece p covers KPI keys of K (p < DMA_PER_STAGE/2)
+    // or of V; lane l moves chunk (l % CH) ^ swizzle(key) of key (l / CH) of
+    // the piece, so the piece lands in LDS already permuted.  A unit with fewer
+    // than 64 valid keys clamps each lane's key to its last valid one.
+    constexpr int PK_HALF = C::DMA_PER_STAGE / 2;
+    const bool dma_v = w * C::DMA_PER_WAVE >= PK_HALF;
+    const int pk0 = w * C::DMA_PER_WAVE - (dma_v ? PK_HALF : 0);
+    const int strideB = (int)(stride * 2);
+    auto issue_stage = [&](int st) {
+        const UnitInfo ui = unit_info(a, vi, upre, tab_start, tab_nlen, id.g, u0 + st);
+        const uint16_t* kb = (ui.stream < 0 ? kpre : kev) + ui.key_off;
+        const uint16_t* vb = (ui.stream < 0 ? vpre : vev) + ui.key_off;
+        const unsigned char* base = reinterpret_cast<const unsigned char*>(dma_v ? vb : kb);
+        const uint32_t ldsb =
+            lds_u32(lds + (st % C::NSTAGE) * C::STAGE + (dma_v ? C::STAGE_K : 0) + pk0 * 1024);
+        const int clamp = ui.nk - 1;
+#pragma unroll
+        for (int i = 0; i < C::DMA_PER_WAVE; ++i) {
+            const int key = (pk0 + i) * C::KPI + lane / C::CH;
+            const int slot = lane % C::CH;
+            const int ch = dma_v ? (slot ^ ((2 * key) & C::VSW)) : (slot ^ (key % C::CH));
+            const uint32_t off = (uint32_t)(min(key, clamp) * strideB + 16 * ch);
+            dma_16B_sbase(base, off, ldsb + 1024 * i);
+        }
+    };
+
+    // The first three stages go out before the query rows are read, so the
+    // ring fills while those loads are in flight.
+#pragma unroll
+    for (int st = 0; st < C::NSTAGE - 1; ++st)
+        if (st < nstages) issue_stage(st);
+
     // rows of this lane: 16*(rw*NT+nt) + l16 within the item, stream-major
     const int wrow0 = row0 + 16 * rw * NT;                // first video row of this wave
     const bool row_wave_active = 16 * rw * NT < nrows;
@@ -235,30 +268,6 @@ __global__ __launch_bounds__(64 * WR * WK) void split_mfma_kernel(StepArgs a)
         w_str_lo = __builtin_amdgcn_readfirstlane(w_str_lo);
         w_str_hi = __builtin_amdgcn_readfirstlane(w_str_hi);
     }
-
-    // DMA of one stage (unit u0 + st): this wave's DMA_PER_WAVE 1 KB pieces.
-    // Piece p covers KPI keys of K (p < DMA_PER_STAGE/2) or of V; lane l
-    // moves chunk (l % CH) ^ swizzle(key) of key (l / CH) of the piece, so the
-    // piece lands in LDS already permuted.
-    auto issue_stage = [&](int st) {
-        const UnitInfo ui = unit_info(a, vi, upre, tab_start, tab_nlen, id.g, u0 + st);
-        const uint16_t* kb = (ui.stream < 0 ? kpre : kev) + ui.key_off;
-        const uint16_t* vb = (ui.stream < 0 ? vpre : vev) + ui.key_off;
-        unsigned char* sbase = lds + (st % C::NSTAGE) * C::STAGE;
-#pragma unroll
-        for (int i = 0; i < C::DMA_PER_WAVE; ++i) {
-            const int piece = w * C::DMA_PER_WAVE + i;
-            const bool is_v = piece >= C::DMA_PER_STAGE / 2;
-            const int pk = is_v ? piece - C::DMA_PER_STAGE / 2 : piece;
-            const int key = pk * C::KPI + lane / C::CH;
-            const int slot = lane % C::CH;
-            const int ch = is_v ? (slot ^ ((2 * key) & C::VSW)) : (slot ^ (key % C::CH));
-            const int gkey = min(key, ui.nk - 1);
-            const uint16_t* src = (is_v ? vb : kb) + (long)gkey * stride + 8 * ch;
-            unsigned char* dst = sbase + (is_v ? C::STAGE_K : 0) + pk * 1024;
-            dma_16B(src, lds_u32(dst));
-        }
-    };
 
     // The row normaliser is one more matrix product per block, ones^T P^T:
     // its accumulator holds the row sum of the block's bf16 P (the same P
@@ -400,10 +409,6 @@ __global__ __launch_bounds__(64 * WR * WK) void split_mfma_kernel(StepArgs a)
             for (int nt = 0; nt < NT; ++nt) o[nt][dt] = mfma_16x16x32(vf, pf[nt], o[nt][dt]);
         }
     };
-
-#pragma unroll
-    for (int st = 0; st < C::NSTAGE - 1; ++st)
-        if (st < nstages) issue_stage(st);
 
     for (int st = 0; st < nstages; ++st) {
         // after the barrier every wave's pieces of stage st have landed and

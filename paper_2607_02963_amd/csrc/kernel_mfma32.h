@@ -84,27 +84,6 @@ __device__ inline int m32_vswz(int key)
     return (6 * (k & 1)) ^ (12 * (k >> 1));
 }
 
-// One wave-wide 16-byte-per-lane DMA into LDS from a scalar base address
-// plus a per-lane 32-bit byte offset: lane l's 16 bytes land at lds_base +
-// 16 l.  The address arithmetic of a stage is then a few scalar
-// instructions instead of 64-bit vector adds per lane.
-__device__ inline void dma_16B_sbase(const void* base, uint32_t off, uint32_t lds_base)
-{
-    // the base is uniform over the wave; say so, so that it sits in SGPRs
-    // (readfirstlane returns int: each half is widened as an unsigned word,
-    // never sign-extended)
-    const uint64_t b = reinterpret_cast<uint64_t>(base);
-    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)b);
-    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(b >> 32));
-    const uint64_t sb = ((uint64_t)hi << 32) | (uint64_t)lo;
-    base = reinterpret_cast<const void*>(sb);
-    uint32_t saved;
-    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %2, %3\n\ts_mov_b32 m0, %0"
-                 : "=&s"(saved)
-                 : "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(off), "s"(base)
-                 : "memory");
-}
-
 // Where one wave's DMA pieces of unit u go (see split_m32_kernel): the
 // unit's first key row of the wave's tensor (K for waves 0..3, V for 4..7),
 // the LDS address of its first piece, the unit's valid keys and the number of

@@ -359,7 +359,7 @@ int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_pr
     if (ev_stop && hipEventRecord(ev_stop, s) != hipSuccess) return PDEC_ERR_HIP;
     // one chunk per row on the matrix-core path: the split pass wrote the result
     if (p.path == kPathMfma && p.max_chunks == 1) return PDEC_OK;
-    const int fgrid = (int)rows;
+    const int fgrid = (int)ceil_div(rows, 4);  // four rows per work-group
     const dim3 fblock(256);
     if (bf16) {
         if (d->head_dim == 128) hipLaunchKernelGGL((finish_kernel<uint16_t, 128>), dim3(fgrid), fblock, 0, s, a);

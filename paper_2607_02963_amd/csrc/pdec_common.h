@@ -271,6 +271,27 @@ __device__ inline void dma_16B(const void* src, uint32_t lds_base)
                  : "memory");
 }
 
+// One wave-wide 16-byte-per-lane DMA into LDS from a scalar base address
+// plus a per-lane 32-bit byte offset: lane l's 16 bytes land at lds_base +
+// 16 l.  The address arithmetic of a stage is then a few scalar
+// instructions instead of 64-bit vector adds per lane.
+__device__ inline void dma_16B_sbase(const void* base, uint32_t off, uint32_t lds_base)
+{
+    // the base is uniform over the wave; say so, so that it sits in SGPRs
+    // (readfirstlane returns int: each half is widened as an unsigned word,
+    // never sign-extended)
+    const uint64_t b = reinterpret_cast<uint64_t>(base);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)b);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(b >> 32));
+    const uint64_t sb = ((uint64_t)hi << 32) | (uint64_t)lo;
+    base = reinterpret_cast<const void*>(sb);
+    uint32_t saved;
+    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %2, %3\n\ts_mov_b32 m0, %0"
+                 : "=&s"(saved)
+                 : "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(off), "s"(base)
+                 : "memory");
+}
+
 // Wait until at most N of this wave's vector-memory operations are in flight
 // and its LDS operations are done, then barrier the work-group.  Written as
 // one asm statement so the compiler neither drains every DMA nor moves LDS
