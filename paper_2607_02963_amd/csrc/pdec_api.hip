@@ -276,14 +276,13 @@ int debug_check_lengths(const pdec_dims* d, int num_videos, const int32_t* event
                          cu_prefix ? ce.data() : nullptr);
 }
 
-int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_prefix, const void* v_prefix,
-             const int32_t* cu_prefix, const int32_t* prefix_len, const void* k_event, const void* v_event,
-             const int32_t* event_lens, const int32_t* cu_events, void* out, float* lse, void* workspace,
-             size_t workspace_bytes, void* stream)
+// Null and alignment checks of a step's arguments (the workspace aside).
+int check_step_pointers(const pdec_dims* d, const void* q, const void* k_prefix, const void* v_prefix,
+                        const int32_t* cu_prefix, const int32_t* prefix_len, const void* k_event,
+                        const void* v_event, const int32_t* event_lens, const int32_t* cu_events, const void* out,
+                        const float* lse)
 {
-    int rc = validate_dims(d, num_videos);
-    if (rc != PDEC_OK) return rc;
-    const void* ptrs[] = {q, k_event, v_event, out, workspace};
+    const void* ptrs[] = {q, k_event, v_event, out};
     for (const void* p : ptrs)
         if (!p || !aligned16(p)) return PDEC_ERR_INVALID_ARG;
     // an empty prefix (max_prefix_len == 0) may come as null pointers
@@ -296,6 +295,20 @@ int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_pr
     } else if (!prefix_len || !aligned4(prefix_len)) {
         return PDEC_ERR_INVALID_ARG;
     }
+    return PDEC_OK;
+}
+
+int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_prefix, const void* v_prefix,
+             const int32_t* cu_prefix, const int32_t* prefix_len, const void* k_event, const void* v_event,
+             const int32_t* event_lens, const int32_t* cu_events, void* out, float* lse, void* workspace,
+             size_t workspace_bytes, void* stream)
+{
+    int rc = validate_dims(d, num_videos);
+    if (rc != PDEC_OK) return rc;
+    if (!workspace || !aligned16(workspace)) return PDEC_ERR_INVALID_ARG;
+    rc = check_step_pointers(d, q, k_prefix, v_prefix, cu_prefix, prefix_len, k_event, v_event, event_lens,
+                             cu_events, out, lse);
+    if (rc != PDEC_OK) return rc;
     const Plan p = make_plan(d, num_videos);
     if (workspace_bytes < p.ws_bytes) return PDEC_ERR_WORKSPACE;
     if (8 * ceil_div(p.n_items, 8) > (long)INT32_MAX) return PDEC_ERR_UNSUPPORTED;
@@ -408,8 +421,11 @@ int pdec_attn_step_noalloc(const pdec_dims* dims, const void* q, const void* k_p
                            const void* k_event, const void* v_event, const int32_t* event_lens,
                            const int32_t* prefix_lens, void* out, float* lse, void* stream)
 {
-    // size check first: nothing touches the device for a refused call
-    const int rc = validate_dims(dims, 1);
+    // argument and size checks first: nothing touches the device for a refused call
+    int rc = validate_dims(dims, 1);
+    if (rc != PDEC_OK) return rc;
+    rc = check_step_pointers(dims, q, k_prefix, v_prefix, nullptr, prefix_lens, k_event, v_event, event_lens,
+                             nullptr, out, lse);
     if (rc != PDEC_OK) return rc;
     if (make_plan(dims, 1).ws_bytes > PDEC_NOALLOC_SCRATCH_BYTES) return PDEC_ERR_SCRATCH;
     void* ws = scratch_address();
