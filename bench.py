@@ -221,13 +221,28 @@ def run_read_probe(args, torch, pdec):
                       "results": rows}), flush=True)
 
 
+def loop_split_bytes(lp, s: int) -> int:
+    """Algorithmic bytes of the split pass at step s of a decode loop: the
+    prefix K/V once per kv head, each live stream's s + 1 own K/V rows and
+    its q rows."""
+    live = int((s < lp.eos_step).sum())
+    row = lp.H_kv * lp.D * 2
+    return 2 * lp.prefix_len * row + 2 * live * (s + 1) * row + live * lp.H_q * lp.D * 2
+
+
 def run_loop(args, torch, pdec, wl):
-    """Row a6: the event-parallel decode loop (append + attention per step)
-    against the single-stream sequential decode of the same tokens.  Steps
-    after every stream has ended are not run (no stream issues a token).
-    Two timings: per-step HIP events with a 512 MB cache flush before each
-    step (outside the timed region), summed; and the whole loop back to back
-    (the 33.5 MB prefix then stays in the 256 MB MALL: "mall_hot")."""
+    """Row a6: the event-parallel decode loop against the single-stream
+    sequential decode of the same tokens.  Each step appends every live
+    stream's new row and attends; with the append fused into the step
+    (pdec_decode_step, the two count arrays swapped between steps) and, for
+    comparison, as two calls (pdec_kv_append, then the step).  Steps after
+    every stream has ended are not run.  Timings: per-step HIP events with a
+    512 MB cache flush before each step (outside the timed region), summed,
+    with the split pass of each step timed on its own as well; and the whole
+    loop back to back (the 33.5 MB prefix then stays in the 256 MB MALL:
+    "mall_hot").  Roofline fractions: the steps' algorithmic split-pass
+    bytes over the summed split-pass time, and over the summed step time,
+    against 8 TB/s."""
     lp = wl.loop_64()
     flush = torch.empty(ROTATE_BYTES, dtype=torch.uint8, device="cuda")
 
@@ -241,6 +256,7 @@ def run_loop(args, torch, pdec, wl):
         d["kc"] = torch.zeros((E, lp.cap, lp.H_kv, lp.D), dtype=torch.bfloat16, device="cuda")
         d["vc"] = torch.zeros_like(d["kc"])
         d["lens"] = torch.zeros(E, dtype=torch.int32, device="cuda")
+        d["lens2"] = torch.zeros(E, dtype=torch.int32, device="cuda")
         d["out"] = torch.empty((E, lp.H_q, lp.D), dtype=torch.bfloat16, device="cuda")
         d["lse"] = torch.empty((E, lp.H_q), dtype=torch.float32, device="cuda")
         dims = pdec.make_dims(E, lp.H_q, lp.H_kv, lp.D, lp.cap, lp.prefix_len, pdec.PDEC_DTYPE_BF16)
@@ -248,16 +264,26 @@ def run_loop(args, torch, pdec, wl):
         d["steps"] = int(lp.eos_step.max())
         return d
 
-    def one(d, s):
+    def fused(d, s):
+        pdec.decode_step(d["q"][s], d["kp"], d["vp"], d["kn"][s], d["vn"][s], d["kc"], d["vc"], d["lens"],
+                         d["lens2"], d["live"][s], prefix_lens=d["plen"], out=d["out"], lse=d["lse"],
+                         workspace=d["ws"])
+        d["lens"], d["lens2"] = d["lens2"], d["lens"]
+
+    def two_calls(d, s):
         pdec.kv_append(d["kn"][s], d["vn"][s], d["kc"], d["vc"], d["lens"], d["live"][s])
         pdec.attn_step(d["q"][s], d["kp"], d["vp"], d["kc"], d["vc"], d["lens"], d["plen"], out=d["out"],
                        lse=d["lse"], workspace=d["ws"])
 
-    def timed(d):
+    def reset(d):
         d["lens"].zero_()
+        d["lens2"].zero_()
+
+    def timed(d, one):
+        reset(d)
         for s in range(d["steps"]):  # warm-up pass
             one(d, s)
-        d["lens"].zero_()
+        reset(d)
         torch.cuda.synchronize()
         total = 0.0
         for s in range(d["steps"]):
@@ -268,7 +294,18 @@ def run_loop(args, torch, pdec, wl):
             e1.record()
             e1.synchronize()
             total += e0.elapsed_time(e1)
-        d["lens"].zero_()
+        # the split pass alone, in a pass of its own (its events stay out of the step timing)
+        reset(d)
+        torch.cuda.synchronize()
+        timer = pdec.SplitTimer(d["steps"])
+        with timer:
+            for s in range(d["steps"]):
+                flush.fill_(s & 255)
+                one(d, s)
+                torch.cuda.synchronize()
+        split = sum(timer.durations_ms(d["steps"])) * 1e3
+        timer.close()
+        reset(d)
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
@@ -276,25 +313,49 @@ def run_loop(args, torch, pdec, wl):
             one(d, s)
         e1.record()
         torch.cuda.synchronize()
-        return total * 1e3, e0.elapsed_time(e1) * 1e3
+        return dict(us=total * 1e3, mall_hot_us=e0.elapsed_time(e1) * 1e3, split_us=split)
+
+    def fracs(lp, steps, t):
+        b = sum(loop_split_bytes(lp, s) for s in range(steps))
+        return dict(algorithmic_bytes=b, split_hbm_frac=round(b / (t["split_us"] * 1e-6) / 8e12, 4),
+                    step_hbm_frac=round(b / (t["us"] * 1e-6) / 8e12, 4))
 
     par = setup(lp)
-    par_us, par_hot = timed(par)
-    _log(f"bench: loop {par['steps']} steps: {par_us:.1f} us flushed, {par_hot:.1f} us back to back")
-    seq = setup(lp.sequential())
-    seq_us, seq_hot = timed(seq)
-    _log(f"bench: sequential {seq['steps']} steps: {seq_us:.1f} us flushed, {seq_hot:.1f} us back to back")
+    tf = timed(par, fused)
+    t2 = timed(par, two_calls)
+    _log(f"bench: loop {par['steps']} steps fused: {tf['us']:.1f} us flushed ({tf['split_us']:.1f} us split), "
+         f"{tf['mall_hot_us']:.1f} us back to back; two calls: {t2['us']:.1f} us flushed, "
+         f"{t2['mall_hot_us']:.1f} us back to back")
+    seq_lp = lp.sequential()
+    seq = setup(seq_lp)
+    ts = timed(seq, fused)
+    _log(f"bench: sequential {seq['steps']} steps fused: {ts['us']:.1f} us flushed ({ts['split_us']:.1f} us split), "
+         f"{ts['mall_hot_us']:.1f} us back to back")
+    fp, fs = fracs(lp, par["steps"], tf), fracs(seq_lp, seq["steps"], ts)
     rec = {
         "metric": "us per event-parallel decode loop (append + attention), prefix 16384, 16 streams, EOS U{16..64}",
-        "value": round(par_us, 1), "unit": "us/loop", "n_gpus": 1, "higher_is_better": False, "dtype": "bf16",
+        "value": round(tf["us"], 1), "unit": "us/loop", "n_gpus": 1, "higher_is_better": False, "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": lp.name, "prefix_len": lp.prefix_len, "streams": lp.num_events, "H_q": lp.H_q,
                    "H_kv": lp.H_kv, "head_dim": lp.D, "seed": lp.seed, "steps_run": par["steps"],
-                   "tokens": int(lp.eos_step.sum())},
-        "mall_hot_us": round(par_hot, 1),
-        "sequential": {"steps": seq["steps"], "us": round(seq_us, 1), "mall_hot_us": round(seq_hot, 1)},
-        "speedup_vs_sequential": round(seq_us / par_us, 2),
-        "tokens_per_s": round(int(lp.eos_step.sum()) / (par_us * 1e-6), 1),
+                   "tokens": int(lp.eos_step.sum()), "append": "fused into the step (pdec_decode_step)"},
+        "us_per_step": round(tf["us"] / par["steps"], 2),
+        "mall_hot_us": round(tf["mall_hot_us"], 1),
+        "split_us_per_step": round(tf["split_us"] / par["steps"], 2),
+        "roofline": {"bound": "hbm", "peak": 8000.0, "unit": "GB/s", "split_frac": fp["split_hbm_frac"],
+                     "step_frac": fp["step_hbm_frac"],
+                     "algorithmic_bytes": fp["algorithmic_bytes"],
+                     "note": "algorithmic split-pass bytes summed over the steps, over the summed split-pass "
+                             "time (split_frac) and the summed step time (step_frac)"},
+        "two_calls": {"us": round(t2["us"], 1), "us_per_step": round(t2["us"] / par["steps"], 2),
+                      "mall_hot_us": round(t2["mall_hot_us"], 1)},
+        "sequential": {"steps": seq["steps"], "us": round(ts["us"], 1), "us_per_step": round(ts["us"] / seq["steps"], 2),
+                       "mall_hot_us": round(ts["mall_hot_us"], 1),
+                       "split_us_per_step": round(ts["split_us"] / seq["steps"], 2),
+                       "roofline": {"split_frac": fs["split_hbm_frac"], "step_frac": fs["step_hbm_frac"],
+                                    "algorithmic_bytes": fs["algorithmic_bytes"]}},
+        "speedup_vs_sequential": round(ts["us"] / tf["us"], 2),
+        "tokens_per_s": round(int(lp.eos_step.sum()) / (tf["us"] * 1e-6), 1),
     }
     print(json.dumps(rec), flush=True)
 

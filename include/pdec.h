@@ -180,6 +180,40 @@ int pdec_attn_step_ragged(const pdec_dims* dims, int32_t num_videos, const void*
                           size_t workspace_bytes, void* stream);
 
 /*
+ * A decode step with the cache append fused into it (§3.4: at each step every
+ * live stream appends its own new token and attends; a stream that has
+ * emitted EOS stops while the others go on).  Equivalent to pdec_kv_append
+ * followed by a step call, bit for bit, in one pass over the caches:
+ *   - lens_in[e] holds the counts BEFORE this step's append.  For a stream
+ *     with live[e] != 0 (every stream when live is NULL) whose cache has
+ *     room, lens_in[e] < event_cap, the step attends lens_in[e] + 1 own rows,
+ *     the last being k_new[e] / v_new[e], which are also written into cache
+ *     row lens_in[e]; a live stream with a full cache attends its
+ *     lens_in[e] rows and appends nothing; a stream with live[e] == 0 has
+ *     ended (out row 0, lse -inf).
+ *   - lens_out[e] receives the counts after the append (lens_in[e] + 1, the
+ *     same, or 0 for an ended stream).  lens_out must not be lens_in: no
+ *     work-group reads a count another one writes, so a loop swaps the two
+ *     arrays between steps.
+ *   - k_new, v_new [E, H_kv, D] device, 16-byte aligned, read;
+ *     k_event, v_event [E, event_cap, H_kv, D] device, read, and row
+ *     lens_in[e] of every appending stream written;  live [E] int32 or NULL.
+ *   - One video: num_videos 1, prefix_lens [1] device, cu_prefix and
+ *     cu_events NULL.  A batch: cu_prefix and cu_events as for
+ *     pdec_attn_step_ragged, prefix_lens ignored.
+ *   - q, k_prefix, v_prefix, out, lse, workspace as for pdec_attn_step.
+ * dims->queries_per_stream must be 0 or 1 (else PDEC_ERR_UNSUPPORTED).  The
+ * 32-row-tile kernels (pdec_set_path(3)) are not used by this call.
+ * PDEC_DEBUG=1 checks lens_in.  Asynchronous on `stream`.  Returns a
+ * pdec_status.
+ */
+int pdec_decode_step(const pdec_dims* dims, int32_t num_videos, const void* q, const void* k_prefix,
+                     const void* v_prefix, const int32_t* prefix_lens, const int32_t* cu_prefix,
+                     const int32_t* cu_events, const void* k_new, const void* v_new, void* k_event, void* v_event,
+                     const int32_t* lens_in, int32_t* lens_out, const int32_t* live, void* out, float* lse,
+                     void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * Per-stream cache append before a step (§3.4: each live stream extends its
  * own subchain; App. B.5: the total cache does not grow beyond what
  * sequential decoding would hold).  For every stream e with live[e] != 0

@@ -29,16 +29,18 @@ namespace pdec {
 
 constexpr int kMaxChunks = 512;  // largest slot count per row the host plans
 
+typedef __attribute__((ext_vector_type(4))) uint32_t fin_u32x4_t;
+
 template <typename T, int D>
 __global__ __launch_bounds__(256) void finish_kernel(StepArgs a)
 {
+    using u32x4_t = fin_u32x4_t;
     constexpr int EPL = 16 / (int)sizeof(T);  // elements per lane and slot
     constexpr int LPS = D / EPL;              // lanes per slot
     constexpr int SPI = 64 / LPS;             // slots per wave instruction
     constexpr int NB = 64 / SPI < 16 ? 64 / SPI : 16;  // slots per lane and batch
     constexpr int BATCH = SPI * NB;
     static_assert(LPS * EPL == D && SPI * LPS == 64, "head_dim 64 or 128");
-    typedef __attribute__((ext_vector_type(4))) uint32_t u32x4_t;
 
     const int wave = threadIdx.x >> 6;
     const int lane = threadIdx.x & 63;
@@ -50,7 +52,30 @@ __global__ __launch_bounds__(256) void finish_kernel(StepArgs a)
     const int d0 = EPL * (lane % LPS);
     T* __restrict__ out = static_cast<T*>(a.out) + qr * D + d0;
 
-    if (a.event_lens[e] <= 0) {  // ended stream: uniform over the wave
+    // Fused append (one query per stream): the wave of the first query head
+    // of kv head g copies stream e's appended K and V rows of head g into the
+    // caches, loading them before the slots and storing them last; the wave
+    // of head 0 writes the advanced count.  No other work item of the step
+    // touches those cache rows or lens_out.
+    const int h = (int)(qr % a.H_q);
+    const int app_n = a.k_new && h % a.G == 0 ? appended_row(a, e) : -1;
+    constexpr int RCH = D * (int)sizeof(T) / 16;  // 16-byte pieces of one row
+    u32x4_t app_x = u32x4_t{0u, 0u, 0u, 0u};
+    unsigned char* app_dst = nullptr;
+    if (app_n >= 0 && lane < 2 * RCH) {
+        const bool is_v = lane >= RCH;
+        const int piece = is_v ? lane - RCH : lane;
+        const long row = ((long)e * a.H_kv + h / a.G) * D * (long)sizeof(T);
+        const unsigned char* nk = static_cast<const unsigned char*>(a.k_new);
+        const unsigned char* nv = static_cast<const unsigned char*>(a.v_new);
+        app_x = *reinterpret_cast<const u32x4_t*>((is_v ? nv : nk) + row + 16 * piece);
+        unsigned char* ck = static_cast<unsigned char*>(const_cast<void*>(a.k_event));
+        unsigned char* cv = static_cast<unsigned char*>(const_cast<void*>(a.v_event));
+        app_dst = (is_v ? cv : ck) + (((long)e * a.cap + app_n) * a.H_kv + h / a.G) * D * (long)sizeof(T) + 16 * piece;
+    }
+    if (a.k_new && h == 0 && lane == 0) a.lens_out[e] = stream_len(a, e);
+
+    if (stream_len(a, e) <= 0) {  // ended stream: uniform over the wave
         if (j == 0) *reinterpret_cast<u32x4_t*>(out) = u32x4_t{0u, 0u, 0u, 0u};
         if (a.lse && lane == 0) a.lse[qr] = kNegInf;
         return;
@@ -123,6 +148,7 @@ __global__ __launch_bounds__(256) void finish_kernel(StepArgs a)
         }
         if (a.lse && lane == 0) a.lse[qr] = kLn2 * (M + __log2f(lsum));
     }
+    if (app_dst) *reinterpret_cast<u32x4_t*>(app_dst) = app_x;
 }
 
 }  // namespace pdec

@@ -162,7 +162,13 @@ __global__ __launch_bounds__(64 * WR * WK) void split_mfma_kernel(StepArgs a)
         if (first_item && tid == 0) a.video_chunks[id.v] = min(max((total + upc - 1) / upc, 1), a.max_chunks);
         u1 = min(u1, total);
     }
-    if (u0 >= u1) return;
+    // fused append without a finish pass (one chunk): this item stores the
+    // appended rows of its kv head (else the finish pass does)
+    const bool app_store = a.k_new && a.max_chunks == 1 && id.c == 0 && id.rg == 0;
+    if (u0 >= u1) {
+        if (app_store) fused_append_store(a, vi, id.g, 2);
+        return;
+    }
     int nstages = u1 - u0;
     if constexpr (MQ) {
         // whole branches: rows of one stream f see none of the units after
@@ -200,6 +206,21 @@ __global__ __launch_bounds__(64 * WR * WK) void split_mfma_kernel(StepArgs a)
         const uint32_t ldsb =
             lds_u32(lds + (st % C::NSTAGE) * C::STAGE + (dma_v ? C::STAGE_K : 0) + pk0 * 1024);
         const int clamp = ui.nk - 1;
+        // fused append: a stream's appended row (the last valid key of its
+        // last unit) comes from k_new / v_new instead of the cache
+        const AppendedKey ak = appended_key(a, vi, ui, id.g, 2);
+        if (ak.key >= 0) {
+            const unsigned char* nrow = dma_v ? ak.vrow : ak.krow;
+#pragma unroll
+            for (int i = 0; i < C::DMA_PER_WAVE; ++i) {
+                const int key = (pk0 + i) * C::KPI + lane / C::CH;
+                const int slot = lane % C::CH;
+                const int ch = dma_v ? (slot ^ ((2 * key) & C::VSW)) : (slot ^ (key % C::CH));
+                const int kk = min(key, clamp);
+                dma_16B(kk == ak.key ? nrow + 16 * ch : base + kk * strideB + 16 * ch, ldsb + 1024 * i);
+            }
+            return;
+        }
 #pragma unroll
         for (int i = 0; i < C::DMA_PER_WAVE; ++i) {
             const int key = (pk0 + i) * C::KPI + lane / C::CH;
@@ -450,6 +471,8 @@ __global__ __launch_bounds__(64 * WR * WK) void split_mfma_kernel(StepArgs a)
         }
     }
 
+    if (app_store) fused_append_store(a, vi, id.g, 2);  // every DMA has landed
+
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) l_part[nt] = lsum[nt][0];
 
@@ -508,7 +531,7 @@ __global__ __launch_bounds__(64 * WR * WK) void split_mfma_kernel(StepArgs a)
                 // finish pass, and the row's result is written here with the
                 // finish's arithmetic for one slot (the same bf16 values and
                 // lse), an ended stream giving 0 and -inf.
-                const bool ended = a.event_lens[qr / ((long)a.H_q * a.qps)] <= 0;
+                const bool ended = stream_len(a, (int)(qr / ((long)a.H_q * a.qps))) <= 0;
                 dst = static_cast<uint16_t*>(a.out) + qr * D;
 #pragma unroll
                 for (int dt = 0; dt < C::DT; ++dt) {

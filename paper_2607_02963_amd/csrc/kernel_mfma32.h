@@ -578,7 +578,7 @@ __global__ __launch_bounds__(512) void split_m32_kernel(StepArgs a)
         // A single chunk holds the whole row: the host launches no finish
         // pass, and the row's result is written here with the finish's
         // arithmetic for one slot, an ended stream giving 0 and -inf.
-        ended = a.event_lens[qr / a.H_q] <= 0;
+        ended = a.event_lens[qr / a.H_q] <= 0;  // (no fused append reaches this kernel)
         dst = static_cast<uint16_t*>(a.out) + qr * D;
         if (a.lse && hi == 0) a.lse[qr] = ended ? kNegInf : kLn2 * (m_ref + __log2f(l_row));
     } else if (hi == 0) {

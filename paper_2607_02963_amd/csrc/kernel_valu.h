@@ -304,10 +304,12 @@ __global__ __launch_bounds__(256) void split_valu_bf16_kernel(StepArgs a)
     // K: pass p gives lane (kslot, slice) key p*KPP + kslot, bytes slice*32 .. +32
     auto load_k = [&](const UnitInfo& ui, uint4 (&kx)[NP][2]) {
         const unsigned char* kb = k_base(ui);
+        const AppendedKey ak = appended_key(a, it.vi, ui, it.id.g, 2);  // fused append: key from k_new
 #pragma unroll
         for (int p = 0; p < NP; ++p) {
-            const uint32_t off = (uint32_t)min(p * KPP + kslot, ui.nk - 1) * stride_b + (uint32_t)slice * 32u;
-            const uint4* src = reinterpret_cast<const uint4*>(kb + off);
+            const int kk = min(p * KPP + kslot, ui.nk - 1);
+            const uint32_t off = (uint32_t)kk * stride_b + (uint32_t)slice * 32u;
+            const uint4* src = reinterpret_cast<const uint4*>(kk == ak.key ? ak.krow + slice * 32 : kb + off);
             kx[p][0] = src[0];
             kx[p][1] = src[1];
         }
@@ -324,8 +326,12 @@ __global__ __launch_bounds__(256) void split_valu_bf16_kernel(StepArgs a)
     };
     auto load_v = [&](const UnitInfo& ui, uint32_t (&vw)[kUnit]) {
         const unsigned char* vb = v_base(ui);
+        const AppendedKey ak = appended_key(a, it.vi, ui, it.id.g, 2);  // fused append: key from v_new
 #pragma unroll
-        for (int k = 0; k < kUnit; ++k) vw[k] = load_v1(vb + (size_t)min(k, ui.nk - 1) * stride_b, v_lane);
+        for (int k = 0; k < kUnit; ++k) {
+            const int kk = min(k, ui.nk - 1);
+            vw[k] = load_v1(kk == ak.key ? ak.vrow : vb + (size_t)kk * stride_b, v_lane);
+        }
     };
 
     float m_ref[RT], l_lane[RT], o[RT][DPL];
@@ -505,12 +511,14 @@ __global__ __launch_bounds__(256) void split_valu_f32_kernel(StepArgs a)
         float sx[RT];
 #pragma unroll
         for (int r = 0; r < RT; ++r) sx[r] = 0.f;
-        const uint32_t koff = (uint32_t)min(lane, nk - 1) * stride_b;
+        const AppendedKey ak = appended_key(a, it.vi, ui, it.id.g, 4);  // fused append: key from k_new / v_new
+        const int kk = min(lane, nk - 1);
+        const unsigned char* krow = kk == ak.key ? ak.krow : kb + (uint32_t)kk * stride_b;
 #pragma unroll
         for (int h = 0; h < NH; ++h) {
             uint4 kx[KH];
 #pragma unroll
-            for (int j = 0; j < KH; ++j) kx[j] = *reinterpret_cast<const uint4*>(kb + koff + 16 * (h * KH + j));
+            for (int j = 0; j < KH; ++j) kx[j] = *reinterpret_cast<const uint4*>(krow + 16 * (h * KH + j));
 #pragma unroll
             for (int j = 0; j < KH; ++j) {
                 int jj = h * KH + j;
@@ -553,8 +561,9 @@ __global__ __launch_bounds__(256) void split_valu_f32_kernel(StepArgs a)
             float vf[VB][DPL];
 #pragma unroll
             for (int k = 0; k < VB; ++k) {
+                const int kv = min(k0 + k, nk - 1);
                 const float* src =
-                    reinterpret_cast<const float*>(vb + (size_t)min(k0 + k, nk - 1) * stride_b) + lane * DPL;
+                    reinterpret_cast<const float*>(kv == ak.key ? ak.vrow : vb + (size_t)kv * stride_b) + lane * DPL;
 #pragma unroll
                 for (int j = 0; j < DPL; ++j) vf[k][j] = src[j];
             }

@@ -298,10 +298,18 @@ int check_step_pointers(const pdec_dims* d, const void* q, const void* k_prefix,
     return PDEC_OK;
 }
 
+// The append fused into a step (pdec_decode_step).
+struct FusedAppend {
+    const void* k_new;
+    const void* v_new;
+    const int32_t* live;
+    int32_t* lens_out;
+};
+
 int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_prefix, const void* v_prefix,
              const int32_t* cu_prefix, const int32_t* prefix_len, const void* k_event, const void* v_event,
              const int32_t* event_lens, const int32_t* cu_events, void* out, float* lse, void* workspace,
-             size_t workspace_bytes, void* stream)
+             size_t workspace_bytes, void* stream, const FusedAppend* fa = nullptr)
 {
     int rc = validate_dims(d, num_videos);
     if (rc != PDEC_OK) return rc;
@@ -309,7 +317,16 @@ int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_pr
     rc = check_step_pointers(d, q, k_prefix, v_prefix, cu_prefix, prefix_len, k_event, v_event, event_lens,
                              cu_events, out, lse);
     if (rc != PDEC_OK) return rc;
-    const Plan p = make_plan(d, num_videos);
+    if (fa) {
+        // one query per stream only; counts in and out in different arrays
+        if (d->queries_per_stream > 1) return PDEC_ERR_UNSUPPORTED;
+        if (!fa->k_new || !fa->v_new || !aligned16(fa->k_new) || !aligned16(fa->v_new) || !fa->lens_out ||
+            !aligned4(fa->lens_out) || (fa->live && !aligned4(fa->live)) || fa->lens_out == event_lens)
+            return PDEC_ERR_INVALID_ARG;
+    }
+    Plan p = make_plan(d, num_videos);
+    // the 32-row-tile kernels read no appended rows: a fused step keeps 16-row tiles
+    if (fa && p.shape >= 4) p.shape = p.shape == 5 ? 2 : 3;
     if (workspace_bytes < p.ws_bytes) return PDEC_ERR_WORKSPACE;
     if (8 * ceil_div(p.n_items, 8) > (long)INT32_MAX) return PDEC_ERR_UNSUPPORTED;
     if (debug_mode() &&
@@ -352,6 +369,12 @@ int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_pr
     a.plan_T = d->plan_mask ? d->plan_tokens_per_stream : 0;
     a.qps = std::max(d->queries_per_stream, 1);
     a.cross = d->cross_causal;
+    if (fa) {
+        a.k_new = fa->k_new;
+        a.v_new = fa->v_new;
+        a.live = fa->live;
+        a.lens_out = fa->lens_out;
+    }
 
     hipStream_t s = static_cast<hipStream_t>(stream);
     const int grid = 8 * a.items_per_xcd;
@@ -442,6 +465,20 @@ int pdec_attn_step_ragged(const pdec_dims* dims, int32_t num_videos, const void*
     if (!cu_prefix || !cu_events) return PDEC_ERR_INVALID_ARG;
     return run_step(dims, num_videos, q, k_prefix, v_prefix, cu_prefix, nullptr, k_event, v_event, event_lens,
                     cu_events, out, lse, workspace, workspace_bytes, stream);
+}
+
+int pdec_decode_step(const pdec_dims* dims, int32_t num_videos, const void* q, const void* k_prefix,
+                     const void* v_prefix, const int32_t* prefix_lens, const int32_t* cu_prefix,
+                     const int32_t* cu_events, const void* k_new, const void* v_new, void* k_event, void* v_event,
+                     const int32_t* lens_in, int32_t* lens_out, const int32_t* live, void* out, float* lse,
+                     void* workspace, size_t workspace_bytes, void* stream)
+{
+    // one video: prefix_lens; a batch: cu_prefix and cu_events (both or neither)
+    if ((cu_prefix == nullptr) != (cu_events == nullptr)) return PDEC_ERR_INVALID_ARG;
+    if (!cu_prefix && num_videos != 1) return PDEC_ERR_INVALID_ARG;
+    const FusedAppend fa{k_new, v_new, live, lens_out};
+    return run_step(dims, num_videos, q, k_prefix, v_prefix, cu_prefix, cu_prefix ? nullptr : prefix_lens, k_event,
+                    v_event, lens_in, cu_events, out, lse, workspace, workspace_bytes, stream, &fa);
 }
 
 int pdec_kv_append(const pdec_dims* dims, const void* k_new, const void* v_new, void* k_event, void* v_event,

@@ -62,6 +62,16 @@ struct StepArgs {
     int plan_T;                 // plan tokens per stream when the self-only plan mask is on, else 0
     int qps;                    // queries per stream: 1 for a decode step, N for whole branches
     int cross;                  // whole branches: other streams' rows at earlier positions visible
+    // Append fused into the step (pdec_decode_step), else k_new == null:
+    // event_lens then holds the counts before the append, the step attends
+    // as after it, reading each appended row from k_new/v_new, and the
+    // finish pass (or, without one, the first chunk's item of every kv head)
+    // stores those rows into the caches and the advanced counts into
+    // lens_out.
+    const void* k_new;          // [SE, H_kv, D] or null
+    const void* v_new;          // [SE, H_kv, D]
+    const int32_t* live;        // [SE] or null (every stream live)
+    int32_t* lens_out;          // [SE]
 };
 
 // Launch of the matrix-core split pass (its own translation unit).
@@ -135,6 +145,55 @@ __device__ inline ItemId item_id(const StepArgs& a, int item)
     return id;
 }
 
+// Cache row that stream e appends at this step (fused append only; §3.4:
+// a live stream extends its own cache, an ended one stops), or -1: no
+// append, a stream that has ended, or a full cache.
+__device__ inline int appended_row(const StepArgs& a, int e)
+{
+    if (!a.k_new || (a.live && a.live[e] == 0)) return -1;
+    const int n = a.event_lens[e];
+    return n >= 0 && n < a.cap ? n : -1;
+}
+
+// Rows of stream e's own cache that the step attends (n_e, the current
+// token included); 0 for a stream that has ended.
+__device__ inline int stream_len(const StepArgs& a, int e)
+{
+    if (!a.k_new) return a.event_lens[e];
+    if (a.live && a.live[e] == 0) return 0;
+    return a.event_lens[e] + (appended_row(a, e) >= 0 ? 1 : 0);
+}
+
+// Fused append on a step without a finish pass, by the first chunk's item
+// of kv head g of a video (the caller tests that): the appended K and V rows
+// of head g go into the caches, and for g = 0 the advanced counts into
+// lens_out.  No work item of
+// the same step reads a cache row written here (the step reads appended rows
+// from k_new/v_new) nor a count in lens_out.  Plain loads and stores: the
+// caller has no DMA in flight.
+__device__ inline void fused_append_store(const StepArgs& a, const VideoInfo& vi, int g, int esz)
+{
+    const int tid = threadIdx.x, nthr = blockDim.x;
+    const int chunks = a.D * esz / 16;  // 16-byte pieces of one row
+    const long rowb = (long)a.D * esz;
+    typedef __attribute__((ext_vector_type(4))) uint32_t u32x4_t;
+    for (int i = tid; i < vi.E * 2 * chunks; i += nthr) {
+        const int f = i / (2 * chunks), r = i - f * 2 * chunks;
+        const bool is_v = r >= chunks;
+        const int ch = is_v ? r - chunks : r;
+        const int e = vi.e0 + f;
+        const int n = appended_row(a, e);
+        if (n < 0) continue;
+        const unsigned char* src =
+            static_cast<const unsigned char*>(is_v ? a.v_new : a.k_new) + ((long)e * a.H_kv + g) * rowb + 16 * ch;
+        unsigned char* dst = static_cast<unsigned char*>(const_cast<void*>(is_v ? a.v_event : a.k_event)) +
+                             (((long)e * a.cap + n) * a.H_kv + g) * rowb + 16 * ch;
+        *reinterpret_cast<u32x4_t*>(dst) = *reinterpret_cast<const u32x4_t*>(src);
+    }
+    if (g == 0)
+        for (int f = tid; f < vi.E; f += nthr) a.lens_out[vi.e0 + f] = stream_len(a, vi.e0 + f);
+}
+
 // Per-video unit table, built in LDS by wave 0 of a work-group:
 //   start[f] = first own unit of stream f (relative to the first own unit),
 //   nlen[f]  = n_f (<= 0 stored as 0); start[E] = total own units.
@@ -145,7 +204,7 @@ __device__ inline int build_unit_table(const StepArgs& a, const VideoInfo& vi, i
     int base = 0;
     for (int f0 = 0; f0 < vi.E; f0 += 64) {
         const int f = f0 + lane;
-        const int n = f < vi.E ? max(a.event_lens[vi.e0 + f], 0) : 0;
+        const int n = f < vi.E ? max(stream_len(a, vi.e0 + f), 0) : 0;
         const int units = (n + kUnit - 1) / kUnit;
         int incl = units;
 #pragma unroll
@@ -195,6 +254,28 @@ __device__ inline UnitInfo unit_info(const StepArgs& a, const VideoInfo& vi, int
     ui.stream = lo;
     ui.k0 = t0;
     return ui;
+}
+
+// Fused append: where unit ui holds its stream's appended key (index
+// `key` within the unit, -1 when it holds none) and that key's K and V rows
+// of head g in k_new / v_new.
+struct AppendedKey {
+    int key;
+    const unsigned char* krow;
+    const unsigned char* vrow;
+};
+__device__ inline AppendedKey appended_key(const StepArgs& a, const VideoInfo& vi, const UnitInfo& ui, int g,
+                                           int esz)
+{
+    AppendedKey r{-1, nullptr, nullptr};
+    if (ui.stream < 0) return r;
+    const int n = appended_row(a, vi.e0 + ui.stream);
+    if (n < ui.k0 || n >= ui.k0 + kUnit) return r;
+    const long off = ((long)(vi.e0 + ui.stream) * a.H_kv + g) * a.D * esz;
+    r.key = n - ui.k0;
+    r.krow = static_cast<const unsigned char*>(a.k_new) + off;
+    r.vrow = static_cast<const unsigned char*>(a.v_new) + off;
+    return r;
 }
 
 // Whether prefix key j of a video is hidden from the rows of its stream f.

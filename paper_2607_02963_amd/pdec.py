@@ -32,7 +32,7 @@ EXPORTED = ("pdec_strerror", "pdec_workspace_size", "pdec_attn_step", "pdec_attn
             "pdec_kv_append", "pdec_rope_kv_append", "pdec_set_path", "pdec_query_plan",
             "pdec_set_split_timer", "pdec_describe_plan", "pdec_grounding_workspace_size", "pdec_segment_grounding",
             "pdec_aggregation_workspace_size", "pdec_aggregate", "pdec_backward_workspace_size",
-            "pdec_attn_prefill_backward", "pdec_read_probe", "pdec_check_lengths")
+            "pdec_attn_prefill_backward", "pdec_read_probe", "pdec_check_lengths", "pdec_decode_step")
 
 AGGR_MODES = {"uniform": 0, "learned": 1, "attention": 2}
 
@@ -108,6 +108,9 @@ def lib():
         L.pdec_attn_step_ragged.argtypes = [dp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         L.pdec_kv_append.restype = ctypes.c_int
         L.pdec_kv_append.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp]
+        L.pdec_decode_step.restype = ctypes.c_int
+        L.pdec_decode_step.argtypes = [dp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz,
+                                       vp]
         L.pdec_rope_kv_append.restype = ctypes.c_int
         L.pdec_rope_kv_append.argtypes = [dp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_float, vp]
         gp = ctypes.POINTER(GroundDims)
@@ -427,6 +430,51 @@ def attn_step_ragged(q, k_prefix, v_prefix, cu_prefix, k_event, v_event, event_l
             _dev(workspace, "workspace"), ctypes.c_size_t(workspace.numel() * workspace.element_size()),
             _stream(stream, q.device)]
     _check("pdec_attn_step_ragged", lib().pdec_attn_step_ragged(ctypes.byref(dims), *args))
+    return out, lse
+
+
+def decode_step(q, k_prefix, v_prefix, k_new, v_new, k_event, v_event, lens_in, lens_out, live=None, *,
+                prefix_lens=None, cu_prefix=None, cu_events=None, max_prefix_len=None, max_events_per_video=0,
+                out=None, lse=None, workspace=None, scale=0.0, stream=None, want_lse=True):
+    """A decode step with the cache append fused in (``pdec_decode_step``);
+    returns (out, lse).  ``lens_in`` holds the counts before the append,
+    ``lens_out`` (another tensor) receives them after it; row lens_in[e] of
+    every appending stream's caches receives k_new[e] / v_new[e].  One video:
+    ``prefix_lens`` [1]; a batch: ``cu_prefix`` and ``cu_events`` [V+1]
+    (``max_prefix_len`` then required).  Other arguments as for ``attn_step``.
+    """
+    SE, H_q, D = q.shape
+    H_kv = k_prefix.shape[1]
+    cap = k_event.shape[1]
+    ragged = cu_prefix is not None
+    V = cu_prefix.shape[0] - 1 if ragged else 1
+    if max_prefix_len is None:
+        if ragged:
+            raise ValueError("max_prefix_len is required for a batch")
+        max_prefix_len = k_prefix.shape[0]
+    dims = make_dims(SE, H_q, H_kv, D, cap, max_prefix_len, _dtype_code(q), scale, max_events_per_video,
+                     prefix_tokens=k_prefix.shape[0] if ragged else 0)
+    ws_bytes = workspace_size(dims, V)
+    out, lse, workspace = _outputs(q, out, lse, workspace, ws_bytes)
+    if k_new.shape != (SE, H_kv, D) or v_new.shape != k_new.shape or k_event.shape[0] != SE:
+        raise ValueError("inconsistent append shapes")
+    if v_prefix.shape != k_prefix.shape or v_event.shape != k_event.shape or out.shape != q.shape:
+        raise ValueError("inconsistent K/V shapes")
+    if lens_in.shape[0] != SE or lens_out.shape[0] != SE:
+        raise ValueError("lens shape")
+    args = [ctypes.c_int32(V), _dev(q, "q", ndim=3), _dev(k_prefix, "k_prefix", q.dtype, 3),
+            _dev(v_prefix, "v_prefix", q.dtype, 3),
+            None if ragged else _dev(prefix_lens, "prefix_lens", torch.int32, 1),
+            _dev(cu_prefix, "cu_prefix", torch.int32, 1) if ragged else None,
+            _dev(cu_events, "cu_events", torch.int32, 1) if ragged else None,
+            _dev(k_new, "k_new", q.dtype, 3), _dev(v_new, "v_new", q.dtype, 3),
+            _dev(k_event, "k_event", q.dtype, 4), _dev(v_event, "v_event", q.dtype, 4),
+            _dev(lens_in, "lens_in", torch.int32, 1), _dev(lens_out, "lens_out", torch.int32, 1),
+            None if live is None else _dev(live, "live", torch.int32, 1),
+            _dev(out, "out", q.dtype, 3), _dev(lse, "lse", torch.float32, 2) if want_lse else None,
+            _dev(workspace, "workspace"), ctypes.c_size_t(workspace.numel() * workspace.element_size()),
+            _stream(stream, q.device)]
+    _check("pdec_decode_step", lib().pdec_decode_step(ctypes.byref(dims), *args))
     return out, lse
 
 

@@ -138,6 +138,13 @@ static int refusals(void)
     CHECK(pdec_attn_step_noalloc(&x, NULL, FAKE(1), FAKE(2), FAKE(3), FAKE(4), FAKE(5), FAKE(6), FAKE(7), NULL,
                                  NULL) == PDEC_ERR_INVALID_ARG);
     CHECK(pdec_kv_append(&x, NULL, FAKE(1), FAKE(2), FAKE(3), FAKE(4), NULL, NULL) == PDEC_ERR_INVALID_ARG);
+    /* fused append: counts in and out in one array, a missing new row, half a batch table */
+    CHECK(pdec_decode_step(&x, 1, FAKE(1), FAKE(2), FAKE(3), FAKE(4), NULL, NULL, FAKE(5), FAKE(6), FAKE(7), FAKE(8),
+                           FAKE(9), FAKE(9), NULL, FAKE(10), NULL, FAKE(11), ws, NULL) == PDEC_ERR_INVALID_ARG);
+    CHECK(pdec_decode_step(&x, 1, FAKE(1), FAKE(2), FAKE(3), FAKE(4), NULL, NULL, NULL, FAKE(6), FAKE(7), FAKE(8),
+                           FAKE(9), FAKE(12), NULL, FAKE(10), NULL, FAKE(11), ws, NULL) == PDEC_ERR_INVALID_ARG);
+    CHECK(pdec_decode_step(&x, 2, FAKE(1), FAKE(2), FAKE(3), NULL, FAKE(13), NULL, FAKE(5), FAKE(6), FAKE(7), FAKE(8),
+                           FAKE(9), FAKE(12), NULL, FAKE(10), NULL, FAKE(11), ws, NULL) == PDEC_ERR_INVALID_ARG);
     CHECK(pdec_rope_kv_append(&x, 1, FAKE(1), NULL, FAKE(2), FAKE(3), FAKE(4), FAKE(5), NULL, NULL, FAKE(6), 10000.f,
                               NULL) == PDEC_ERR_INVALID_ARG);
     CHECK(pdec_read_probe(NULL, FAKE(1), 64, 4, 576, 0, FAKE(2), NULL) == PDEC_ERR_INVALID_ARG);

@@ -254,3 +254,23 @@ def test_read_probe_rejects_bad_arguments_before_launch():
     assert L.pdec_read_probe(fake, fake, 0, 4, 576, 0, fake, None) == pdec.PDEC_ERR_INVALID_ARG
     assert L.pdec_read_probe(fake, fake, 64, 4, 576, 2, fake, None) == pdec.PDEC_ERR_INVALID_ARG
     assert L.pdec_read_probe(fake, fake, 64, 4, 100, 1, fake, None) == pdec.PDEC_ERR_INVALID_ARG
+
+
+def test_decode_step_refuses_before_launch():
+    # fake, aligned, never-dereferenced addresses: each call is refused first
+    L = pdec.lib()
+    f = lambda n: ctypes.c_void_p(0x100000 * n)
+    d = _dims()
+    ws = ctypes.c_size_t(pdec.workspace_size(d))
+
+    def call(dims, nv=1, pl=f(4), cp=None, ce=None, kn=f(5), lin=f(9), lout=f(12)):
+        return L.pdec_decode_step(ctypes.byref(dims), nv, f(1), f(2), f(3), pl, cp, ce, kn, f(6), f(7), f(8), lin,
+                                  lout, None, f(10), None, f(11), ws, None)
+
+    assert call(d, lout=f(9)) == pdec.PDEC_ERR_INVALID_ARG         # counts in and out in one array
+    assert call(d, kn=None) == pdec.PDEC_ERR_INVALID_ARG           # no new rows
+    assert call(d, lout=None) == pdec.PDEC_ERR_INVALID_ARG
+    assert call(d, cp=f(13)) == pdec.PDEC_ERR_INVALID_ARG          # cu_prefix without cu_events
+    assert call(d, nv=2) == pdec.PDEC_ERR_INVALID_ARG              # a batch without its tables
+    mq = pdec.make_dims(8, 28, 4, 128, 16, 1024, pdec.PDEC_DTYPE_BF16, queries_per_stream=4)
+    assert call(mq) == pdec.PDEC_ERR_UNSUPPORTED                   # whole branches take no fused append
