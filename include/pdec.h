@@ -258,8 +258,8 @@ int pdec_rope_kv_append(const pdec_dims* dims, int32_t num_videos, void* q, cons
 
 /*
  * Kernel-path selection for the shared-prefix pass, for tests and tuning:
- * 0 = automatic (bfloat16 with >= 16 query rows per key/value head uses the
- * matrix-core kernel, everything else the vector kernel), 1 = always the
+ * 0 = automatic (bfloat16 uses the matrix-core kernel, float32 the vector
+ * kernel), 1 = always the
  * vector kernel, 2 = matrix-core kernel where the type allows it, 3 = as 2,
  * with the decode step at head_dim 128 and more than 64 query rows per kv
  * head on 32-row tiles (kernel shapes 4 and 5) instead of 16-row ones.

@@ -1,4 +1,4 @@
-// Matrix-core split pass (bf16, >= 16 query rows per kv head).
+// Matrix-core split pass (bf16).
 //
 // The prefix part of a step is a dense contraction: for one kv head, every
 // query row of a video (R = E*G of them) against every key of the shared

@@ -72,12 +72,13 @@ def test_workspace_holds_every_partial_slot():
 
 
 @pytest.mark.parametrize("E,G,dt,expect", [(32, 7, pdec.PDEC_DTYPE_BF16, pdec.PATH_MFMA),
-                                            (1, 7, pdec.PDEC_DTYPE_BF16, pdec.PATH_VALU),
+                                            (1, 7, pdec.PDEC_DTYPE_BF16, pdec.PATH_MFMA),
                                             (3, 7, pdec.PDEC_DTYPE_BF16, pdec.PATH_MFMA),
-                                            (2, 7, pdec.PDEC_DTYPE_BF16, pdec.PATH_VALU),
+                                            (2, 7, pdec.PDEC_DTYPE_BF16, pdec.PATH_MFMA),
+                                            (1, 1, pdec.PDEC_DTYPE_BF16, pdec.PATH_MFMA),
                                             (4, 4, pdec.PDEC_DTYPE_F32, pdec.PATH_VALU)])
 def test_dispatch_rule(E, G, dt, expect):
-    """bf16 with >= 16 query rows per kv head -> matrix core, else vector ALUs."""
+    """bf16 -> matrix core at any row count, float32 -> vector ALUs."""
     d = _dims(num_events=E, H_q=G, H_kv=1, dtype_code=dt)
     assert pdec.query_plan(d)[0] == expect
 
@@ -208,7 +209,7 @@ def test_non_positive_scale_selects_the_default_in_forward_and_backward():
 def test_describe_plan_matches_query_plan_and_shapes():
     """pdec_describe_plan agrees with pdec_query_plan and names the
     matrix-core work-group shape by the rows of one kv head (G = 7)."""
-    expect = {7: (1, 64, 1), 16: (2, 128, 1), 32: (3, 256, 1), 64: (3, 256, 2), 2: (0, 8, 2)}
+    expect = {7: (1, 64, 1), 16: (2, 128, 1), 32: (3, 256, 1), 64: (3, 256, 2), 2: (1, 64, 1)}
     for E, (shape, rows, groups) in expect.items():
         d = _dims(num_events=E, max_prefix_len=1100, cap=70)
         info = pdec.describe_plan(d)

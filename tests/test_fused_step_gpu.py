@@ -2,7 +2,8 @@
 calls it replaces, pdec_kv_append then the step, on the same inputs: out,
 lse, both caches and the advanced counts must agree bit for bit.  The cases
 reach every kernel family the fused call can take (the 256-, 128- and
-64-row matrix-core shapes, the bf16 and f32 vector kernels), a ragged batch,
+64-row matrix-core shapes, the latter with a single stream's 7 rows per kv
+head, the bf16 and f32 vector kernels), a ragged batch,
 a step whose single chunk writes the result itself, and a step in which
 nothing is attended; streams that have ended, full caches and empty caches
 are mixed in.  The two-call result is itself checked against the oracle by
@@ -23,7 +24,8 @@ CASES = {
     "mfma128_E16": ("bf16", (2500,), (16,), 28, 4, 128, 24, 0),
     "mfma64_E7": ("bf16", (1500,), (7,), 28, 4, 128, 24, 0),
     "mfma_D64_E12": ("bf16", (1200,), (12,), 16, 2, 64, 20, 0),
-    "valu_bf16_E1": ("bf16", (2000,), (1,), 28, 4, 128, 24, 0),
+    "small_bf16_E1": ("bf16", (2000,), (1,), 28, 4, 128, 24, 0),
+    "valu_bf16_forced_E1": ("bf16", (2000,), (1,), 28, 4, 128, 24, 1),
     "valu_bf16_forced_E9": ("bf16", (900,), (9,), 28, 4, 128, 24, 1),
     "valu_f32_E4": ("f32", (700,), (4,), 8, 2, 128, 16, 0),
     "ragged_3": ("bf16", (1800, 0, 640), (9, 3, 20), 28, 4, 128, 24, 0),

@@ -8,10 +8,10 @@ Ended streams must stay exactly 0 / -inf.  Permuting streams (or query heads
 within a group) must permute the outputs, which also pins the lse indexing.
 
 With 28 query heads over 4 kv heads (G = 7), the stream counts below put
-E*G = 49, 112, 224 and 448 query rows on each kv head: the matrix-core
-kernel's 64-row work-group shape, its 128-row and 256-row shapes on 16-row
-tiles (the automatic choice) and on 32-row tiles, and the 256-row shapes with
-two row groups.  Every case asserts the shape it reaches, and runs on the
+E*G = 14, 49, 112, 224 and 448 query rows on each kv head: the matrix-core
+kernel's 64-row work-group shape with a partly filled and with full row
+tiles, its 128-row and 256-row shapes on 16-row tiles (the automatic choice)
+and on 32-row tiles, and the 256-row shapes with two row groups.  Every case asserts the shape it reaches, and runs on the
 automatic path, on 32-row tiles, and forced onto the vector kernel.
 """
 import numpy as np
@@ -29,8 +29,8 @@ BF16_BIG = wl.bf16_bits(np.array([1e30], np.float32))[0]
 
 # streams -> (kernel shape, rows per item, row groups) on the matrix-core path,
 # automatic (16-row tiles) and on 32-row tiles (above 64 rows)
-SHAPES = {7: (1, 64, 1), 16: (2, 128, 1), 32: (3, 256, 1), 64: (3, 256, 2)}
-SHAPES32 = {7: (1, 64, 1), 16: (5, 128, 1), 32: (4, 256, 1), 64: (4, 256, 2)}
+SHAPES = {2: (1, 64, 1), 7: (1, 64, 1), 16: (2, 128, 1), 32: (3, 256, 1), 64: (3, 256, 2)}
+SHAPES32 = {2: (1, 64, 1), 7: (1, 64, 1), 16: (5, 128, 1), 32: (4, 256, 1), 64: (4, 256, 2)}
 STREAMS = sorted(SHAPES)
 SIDS = [f"E{e}_rows{SHAPES[e][1]}x{SHAPES[e][2]}" for e in STREAMS]
 CAP = 70
@@ -59,8 +59,9 @@ def _lens(E: int) -> list:
     n = rng.integers(1, CAP + 1, size=E)
     n[::5] = 0
     n[1] = CAP
-    n[2] = 1
-    n[3] = 65
+    if E > 3:
+        n[2] = 1
+        n[3] = 65
     return [int(x) for x in n]
 
 

@@ -39,7 +39,7 @@ CASES = [
     ("bf16_comparator_rows7", "bf16", 28, 4, 128, (777,), (1,), (0, 40)),
     ("bf16_d64_mfma", "bf16", 16, 2, 64, (515,), (6,), (0, 9)),
     ("bf16_rows_exactly16", "bf16", 8, 1, 128, (300,), (2,), (0, 5)),
-    ("bf16_rows15_valu", "bf16", 15, 1, 128, (301,), (1,), (0, 5)),
+    ("bf16_rows15", "bf16", 15, 1, 128, (301,), (1,), (0, 5)),
     ("bf16_group32", "bf16", 32, 1, 128, (257,), (3,), (0, 33)),
     ("f32_group32_two_tail_groups", "f32", 32, 1, 64, (200,), (2,), (0, 10)),
     ("f32_d128", "f32", 8, 2, 128, (333,), (3,), (0, 12)),
