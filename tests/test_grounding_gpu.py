@@ -36,6 +36,11 @@ def _check(w, threshold):
     clear = np.abs(ref_sc - cut) > 2 * bound.max(axis=1, keepdims=True)
     assert np.array_equal(got_sal.astype(bool)[clear], ref_sal[clear])
     assert set(np.unique(got_sal)) <= {0, 1}
+    # every flag, near-ties included, is the kernel's float32 decision on its
+    # own scores: score > float32(threshold * max)
+    sc32 = sc.cpu().numpy()
+    cut32 = np.float32(threshold) * sc32.max(axis=1, keepdims=True)
+    assert np.array_equal(got_sal.astype(bool), sc32 > cut32)
     sc2, _ = pdec.segment_grounding(g, p, cu, threshold)
     torch.cuda.synchronize()
     assert torch.equal(sc, sc2)
