@@ -357,7 +357,33 @@ def run_loop(args, torch, pdec, wl):
         "speedup_vs_sequential": round(ts["us"] / tf["us"], 2),
         "tokens_per_s": round(int(lp.eos_step.sum()) / (tf["us"] * 1e-6), 1),
     }
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = loop_cpu_baseline(lp, par["steps"])
     print(json.dumps(rec), flush=True)
+
+
+def loop_cpu_baseline(lp, steps: int, sample_steps: int = 8):
+    """The oracle's decode loop (as it stands) on the host cores: the first
+    sample_steps steps of the loop (every stream still live), scaled to the
+    loop's steps; and one step on one thread, scaled the same way."""
+    sys.path.insert(0, os.path.join(ROOT, "oracle"))
+    import oracle
+    threads = oracle.max_threads()
+    n = min(sample_steps, steps)
+    args = (lp.k_prefix, lp.v_prefix, lp.q_steps[:n], lp.k_new[:n], lp.v_new[:n], lp.eos_step, lp.cap)
+    t0 = time.perf_counter()
+    oracle.decode_loop(*args, threads=threads)
+    dt = (time.perf_counter() - t0) * steps / n
+    t0 = time.perf_counter()
+    oracle.decode_loop(lp.k_prefix, lp.v_prefix, lp.q_steps[:1], lp.k_new[:1], lp.v_new[:1], lp.eos_step, lp.cap,
+                       threads=1)
+    dt1 = (time.perf_counter() - t0) * steps
+    return {"value": round(dt * 1e6, 1), "unit": "us/loop", "cores": threads, "kind": "oracle",
+            "sample": f"the first {n} of the {steps} steps (all {lp.num_events} streams live), float64 dense-mask "
+                      f"oracle with OpenMP over rows, scaled to the loop",
+            "nproc": os.cpu_count(), "omp_max_threads": threads, "cpu_model": _cpu_model(),
+            "single_thread": {"value": round(dt1 * 1e6, 1), "unit": "us/loop", "cores": 1,
+                              "sample": "the first step on one thread, scaled to the loop"}}
 
 
 def run_rope(args, torch, pdec, wl):
