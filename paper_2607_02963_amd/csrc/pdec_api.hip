@@ -165,10 +165,10 @@ Plan make_plan(const pdec_dims* d, int num_videos)
     p.path = path;
     if (path == kPathMfma) {
         // up to 4 tiles of 16 rows -> 8 waves: 1 tile per row wave, 2 key
-        // groups (64 rows); up to 8 -> 8 waves: 2 tiles per row wave, 2 key
-        // groups (128 rows); more -> 256 rows per item: 16 one-tile row
-        // waves (decode step, D = 128) or 8 two-tile row waves (whole
-        // branches, D = 64).  On request the decode step at D = 128 with
+        // groups (64 rows); up to 8 -> 128 rows: 16 waves of one tile x 2
+        // key groups (decode step, D = 128) or 8 waves of 2 tiles x 2 key
+        // groups; more -> 256 rows per item: 16 one-tile row waves (decode
+        // step, D = 128) or 8 two-tile row waves (whole branches, D = 64).  On request the decode step at D = 128 with
         // more than 64 rows runs on 32-row tiles instead (128 rows as 4 row
         // waves x 2 key groups, 256 rows as 8 row waves): half the LDS
         // operand reads, but two waves per SIMD, which hide the memory path

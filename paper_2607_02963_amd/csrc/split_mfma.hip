@@ -31,7 +31,17 @@ void launch_shape(const StepArgs& a, int shape, int grid, hipStream_t s)
     }
     switch (shape) {
     case 1: hipLaunchKernelGGL((split_mfma_kernel<D, 1, 4, 2, PLAN, MQ>), dim3(grid), dim3(512), 0, s, a); break;
-    case 2: hipLaunchKernelGGL((split_mfma_kernel<D, 2, 4, 2, PLAN, MQ>), dim3(grid), dim3(512), 0, s, a); break;
+    case 2:
+        // 128 rows: eight one-tile row waves x two key groups for the decode
+        // step at D = 128 (3-4% faster than four two-tile row waves on the
+        // decode loop and the ragged batch); four two-tile row waves
+        // otherwise (whole branches, D = 64, and the self-only plan mask,
+        // whose sixteen-wave form the compiler gives private memory)
+        if constexpr (D == 128 && !MQ && !PLAN)
+            hipLaunchKernelGGL((split_mfma_kernel<D, 1, 8, 2, PLAN, MQ>), dim3(grid), dim3(1024), 0, s, a);
+        else
+            hipLaunchKernelGGL((split_mfma_kernel<D, 2, 4, 2, PLAN, MQ>), dim3(grid), dim3(512), 0, s, a);
+        break;
     default:
         // 256 rows: sixteen one-tile row waves for the decode step at D = 128
         // (four waves per SIMD hide more latency than eight two-tile waves);
