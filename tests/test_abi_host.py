@@ -275,3 +275,12 @@ def test_decode_step_refuses_before_launch():
     assert call(d, nv=2) == pdec.PDEC_ERR_INVALID_ARG              # a batch without its tables
     mq = pdec.make_dims(8, 28, 4, 128, 16, 1024, pdec.PDEC_DTYPE_BF16, queries_per_stream=4)
     assert call(mq) == pdec.PDEC_ERR_UNSUPPORTED                   # whole branches take no fused append
+
+
+def test_long_single_head_prefix_plans_more_slots_than_one_finish_batch():
+    # the finish pass takes 64 slots per batch at bf16 and 32 at float32; the
+    # parity cases bf16_finish_three_batches / f32_finish_three_batches rely on this
+    bf = pdec.describe_plan(pdec.make_dims(3, 8, 1, 128, 40, 20000, pdec.PDEC_DTYPE_BF16))
+    f32 = pdec.describe_plan(pdec.make_dims(3, 8, 1, 128, 40, 20000, pdec.PDEC_DTYPE_F32))
+    assert bf["merge_pass"] == 1 and bf["max_chunks"] > 128
+    assert f32["merge_pass"] == 1 and f32["max_chunks"] > 64

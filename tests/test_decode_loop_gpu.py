@@ -1,6 +1,7 @@
 """The event-parallel decode loop on the GPU (§3.4: every live stream appends
 its token and attends each step; streams end independently at EOS), checked
-step by step against the oracle's loop, plus the per-stream append itself."""
+step by step against the oracle's loop, with the append as its own call and
+fused into the step, plus the per-stream append itself."""
 import numpy as np
 import pytest
 import torch
@@ -13,7 +14,7 @@ from paper_2607_02963_amd import workloads as wl
 pytestmark = pytest.mark.gpu
 
 
-def run_loop_gpu(lp: wl.LoopInputs):
+def run_loop_gpu(lp: wl.LoopInputs, fused: bool = False):
     E, H_q, H_kv, D, S = lp.num_events, lp.H_q, lp.H_kv, lp.D, lp.steps
     kp, vp = dev_float(lp.k_prefix, lp.dtype), dev_float(lp.v_prefix, lp.dtype)
     q = dev_float(lp.q_steps, lp.dtype)
@@ -27,15 +28,22 @@ def run_loop_gpu(lp: wl.LoopInputs):
     lse = torch.empty((S, E, H_q), dtype=torch.float32, device="cuda")
     dims = pdec.make_dims(E, H_q, H_kv, D, lp.cap, lp.prefix_len, pdec._dtype_code(kp))
     ws = torch.empty(pdec.workspace_size(dims), dtype=torch.uint8, device="cuda")
+    lens2 = torch.full_like(lens, -1)
     for s in range(S):
-        pdec.kv_append(kn[s], vn[s], kc, vc, lens, live[s])
-        pdec.attn_step(q[s], kp, vp, kc, vc, lens, plen, out=out[s], lse=lse[s], workspace=ws)
+        if fused:
+            # the append fused into the step; the two count arrays swap each step
+            pdec.decode_step(q[s], kp, vp, kn[s], vn[s], kc, vc, lens, lens2, live[s], prefix_lens=plen,
+                             out=out[s], lse=lse[s], workspace=ws)
+            lens, lens2 = lens2, lens
+        else:
+            pdec.kv_append(kn[s], vn[s], kc, vc, lens, live[s])
+            pdec.attn_step(q[s], kp, vp, kc, vc, lens, plen, out=out[s], lse=lse[s], workspace=ws)
     torch.cuda.synchronize()
     return host(out), host(lse), lens.cpu().numpy()
 
 
-def _check_loop(lp):
-    out, lse, lens = run_loop_gpu(lp)
+def _check_loop(lp, fused=False):
+    out, lse, lens = run_loop_gpu(lp, fused)
     ref_out, ref_lse = oracle.decode_loop(lp.k_prefix, lp.v_prefix, lp.q_steps, lp.k_new, lp.v_new, lp.eos_step,
                                           cap=lp.cap, scale=lp.scale)
     for s in range(lp.steps):
@@ -56,6 +64,19 @@ def test_small_loop_f32_every_step():
 def test_loop_64_workload_every_step():
     """prefix 16384, 16 streams from empty, EOS steps U{16..64}, 64 steps."""
     _check_loop(wl.loop_64())
+
+
+def test_loop_64_workload_fused_append_every_step():
+    """The same loop through pdec_decode_step, against the oracle's loop."""
+    _check_loop(wl.loop_64(), fused=True)
+
+
+def test_small_loops_fused_append_every_step():
+    _check_loop(wl.make_loop(name="loop_small", L=700, E=5, steps=12, eos_range=(3, 12), seed=1), fused=True)
+    _check_loop(wl.make_loop(name="loop_f32", dtype="f32", H_q=8, H_kv=2, D=64, L=300, E=3, steps=9,
+                             eos_range=(2, 9), sigma=1.0, seed=2), fused=True)
+    lp = wl.make_loop(name="seq_src", L=900, E=3, steps=10, eos_range=(4, 10), seed=3).sequential()
+    _check_loop(lp, fused=True)
 
 
 def test_sequential_comparator_loop():

@@ -48,6 +48,11 @@ CASES = [
     ("bf16_prefix_len1", "bf16", 28, 4, 128, (1,), (3,), (0, 2)),
     ("bf16_prefix_one_block", "bf16", 28, 4, 128, (128,), (3,), (0, 2)),
     ("bf16_many_streams_rows448", "bf16", 28, 4, 128, (640,), (64,), (0, 7)),
+    # one kv head over a long prefix: more chunk slots per row than one
+    # batch of the finish pass holds (158 slots at bf16, 79 at float32), so
+    # the finish folds several batches in with a rescale
+    ("bf16_finish_three_batches", "bf16", 8, 1, 128, (20000,), (3,), (0, 39)),
+    ("f32_finish_three_batches", "f32", 8, 1, 128, (20000,), (3,), (0, 39)),
 ]
 
 
