@@ -320,8 +320,35 @@ def run_loop(args, torch, pdec, wl):
         return dict(algorithmic_bytes=b, split_hbm_frac=round(b / (t["split_us"] * 1e-6) / 8e12, 4),
                     step_hbm_frac=round(b / (t["us"] * 1e-6) / 8e12, 4))
 
+    def graph_loop(d):
+        """The fused loop captured once in a HIP graph and replayed (the
+        counts cleared by eager fills between replays): the loop without the
+        host's per-call work.  Median of 5 replays, MALL warm."""
+        reset(d)
+        torch.cuda.synchronize()
+        lens_a, lens_b = d["lens"], d["lens2"]
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for s in range(d["steps"]):
+                fused(d, s)
+        d["lens"], d["lens2"] = lens_a, lens_b
+        ts = []
+        for _ in range(6):
+            lens_a.zero_()
+            lens_b.zero_()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            graph.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) * 1e3)
+        del graph
+        return float(np.median(ts[1:]))  # the first replay uploads the graph
+
     par = setup(lp)
     tf = timed(par, fused)
+    tg = graph_loop(par)
+    _log(f"bench: loop {par['steps']} steps fused, one HIP graph: {tg:.1f} us back to back")
     t2 = timed(par, two_calls)
     _log(f"bench: loop {par['steps']} steps fused: {tf['us']:.1f} us flushed ({tf['split_us']:.1f} us split), "
          f"{tf['mall_hot_us']:.1f} us back to back; two calls: {t2['us']:.1f} us flushed, "
@@ -341,6 +368,7 @@ def run_loop(args, torch, pdec, wl):
                    "tokens": int(lp.eos_step.sum()), "append": "fused into the step (pdec_decode_step)"},
         "us_per_step": round(tf["us"] / par["steps"], 2),
         "mall_hot_us": round(tf["mall_hot_us"], 1),
+        "graph_us": round(tg, 1),
         "split_us_per_step": round(tf["split_us"] / par["steps"], 2),
         "roofline": {"bound": "hbm", "peak": 8000.0, "unit": "GB/s", "split_frac": fp["split_hbm_frac"],
                      "step_frac": fp["step_hbm_frac"],

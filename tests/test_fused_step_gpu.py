@@ -143,3 +143,61 @@ def test_fused_loop_matches_separate_loop():
         assert torch.equal(_bits(sa), _bits(sb)), t
         assert torch.equal(lens_a, la), t
     assert torch.equal(_bits(kc_a), _bits(kc_b)) and torch.equal(_bits(vc_a), _bits(vc_b))
+
+
+def test_fused_loop_in_a_hip_graph_replays_like_eager():
+    """The fused loop captured in one HIP graph (the library sets no memory
+    with hipMemsetAsync, so nothing of that kind is recorded) and replayed
+    three times, with eager resets of caches and counts between replays:
+    every replay gives bitwise the eager loop's outputs, caches and counts."""
+    lp = wl.make_loop(name="graph_loop", L=1500, E=9, steps=10, eos_range=(3, 10), seed=8)
+    E, S = lp.num_events, lp.steps
+    f = lambda a: dev_float(a, lp.dtype)
+    kp, vp, q, kn, vn = f(lp.k_prefix), f(lp.v_prefix), f(lp.q_steps), f(lp.k_new), f(lp.v_new)
+    live = dev_int(lp.live_mask())
+    plen = dev_int([lp.prefix_len])
+    kc0 = torch.zeros((E, lp.cap, lp.H_kv, lp.D), dtype=kp.dtype, device="cuda")
+    dims = pdec.make_dims(E, lp.H_q, lp.H_kv, lp.D, lp.cap, lp.prefix_len, pdec._dtype_code(kp))
+    ws = torch.empty(pdec.workspace_size(dims), dtype=torch.uint8, device="cuda")
+
+    def state():
+        return dict(kc=kc0.clone(), vc=kc0.clone(), la=torch.zeros(E, dtype=torch.int32, device="cuda"),
+                    lb=torch.zeros(E, dtype=torch.int32, device="cuda"),
+                    out=torch.zeros((S, E, lp.H_q, lp.D), dtype=kp.dtype, device="cuda"),
+                    lse=torch.zeros((S, E, lp.H_q), dtype=torch.float32, device="cuda"))
+
+    def loop(st):
+        a, b = st["la"], st["lb"]
+        for s in range(S):
+            pdec.decode_step(q[s], kp, vp, kn[s], vn[s], st["kc"], st["vc"], a, b, live[s], prefix_lens=plen,
+                             out=st["out"][s], lse=st["lse"][s], workspace=ws)
+            a, b = b, a
+        return a  # the counts after the last step
+
+    ref = state()
+    ref_lens = loop(ref)
+    torch.cuda.synchronize()
+
+    g = state()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        loop(state())  # warm-up off the capture
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        g_lens = loop(g)
+    for rep in range(3):
+        # eager work between replays: restore the caches and clear the counts
+        g["kc"].copy_(kc0)
+        g["vc"].copy_(kc0)
+        g["la"].zero_()
+        g["lb"].zero_()
+        g["out"].zero_()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for what in ("out", "lse", "kc", "vc"):
+            assert torch.equal(_bits(g[what]), _bits(ref[what])), (rep, what)
+        assert torch.equal(g_lens, ref_lens), rep
