@@ -283,10 +283,14 @@ typedef struct pdec_plan_info {
     int32_t rows_per_item; /* query rows of one kv head that one work item serves               */
     int32_t row_groups;    /* work items per (video, kv head, chunk): ceil(rows / rows_per_item)  */
     int32_t chunk_keys;    /* keys of the virtual key sequence per chunk                         */
-    int32_t max_chunks;    /* chunk slots per (video, kv head)                                   */
-    int32_t work_items;    /* work items of the split pass                                       */
+    int32_t max_chunks;    /* partial-state slots per row: the chunks, plus slot 0 of the tail   */
+                           /* pass when tail_blocks > 0                                          */
+    int32_t work_items;    /* work items of the split pass (prefix chunks x row groups x heads) */
     int32_t merge_pass;    /* 1 if partial states are merged after the split pass, else 0 (the  */
                            /* split pass writes out and lse itself)                              */
+    int32_t tail_blocks;   /* work-groups of the per-stream tail pass in the split launch (each */
+                           /* (stream, kv head) pair's G rows against the stream's own keys, 8  */
+                           /* pairs per work-group); 0 when the own keys are chunk units        */
 } pdec_plan_info;
 
 /*

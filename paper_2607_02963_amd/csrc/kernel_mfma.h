@@ -10,10 +10,11 @@
 //
 // Work-group: 8 or 16 waves = WR row waves x WK key groups.  Row wave rw owns NT
 // 16-row tiles; key group kg owns a contiguous 64/WK-key slice of every
-// 64-key stage (one unit).  Keys stream through a 4-stage LDS ring filled by
+// 64-key stage (one unit).  Keys stream through a 3-stage LDS ring filled by
 // global_load_lds_dwordx4 (direct HBM -> LDS DMA, 1 KB per wave
-// instruction, no staging registers), three stages in flight while the
-// fourth is consumed.  Each key row (D bf16) is stored as D/8 16-byte chunks
+// instruction, no staging registers), two stages in flight while the
+// third is consumed; the query rows arrive the same way, ahead of the first
+// stages, so the first stage's products start once it has landed.  Each key row (D bf16) is stored as D/8 16-byte chunks
 // permuted by an XOR of the key index, so the matrix-core operand reads below
 // hit distinct LDS banks (the transposing V read takes 8 keys per 32-lane
 // phase, so the V permutation differs over 8 consecutive keys).
@@ -90,7 +91,10 @@ struct MfmaCfg {
     static constexpr int NW = WR * WK;            // waves
     static constexpr int KS = kUnit;              // keys per stage: one unit
     static constexpr int KW = KS / WK;            // keys per key group per stage
-    static constexpr int NSTAGE = 4;
+    // ring slots: two stages in flight while the third is consumed (a ring
+    // probe streams the decode layout as fast with two stages in flight as
+    // with three or four)
+    static constexpr int NSTAGE = 3;
     static constexpr int ROWB = D * 2;            // bytes per key row
     static constexpr int CH = D / 8;              // 16-byte chunks per key row
     static constexpr int STAGE_K = KS * ROWB;     // bytes of K per stage
@@ -106,6 +110,21 @@ struct MfmaCfg {
     // all banks (over 4 keys at D = 64, whose rows are half a bank period)
     static constexpr int VSW = D == 128 ? 14 : 6;
     static constexpr int LDS = NSTAGE * STAGE;
+    // Query rows come in by DMA too (so that one in-order counter covers them
+    // and the first stages): a wave's QB bytes land in the ring slot of stage
+    // NSTAGE - 1, in the part that the wave's own DMA of that stage refills
+    // (SR bytes), and the rest in an area of their own (XR bytes per wave).
+    static constexpr int QB = NT * 16 * ROWB;
+    static constexpr int SR = STAGE / NW;
+    static constexpr int XR = QB - SR;
+    static constexpr int QX = NW * XR;
+    static_assert(XR >= 0 && SR % 1024 == 0 && XR % 1024 == 0, "query staging");
+    // A tail work-group's eight waves each stage a 32-key K and V block
+    // (TVB bytes each) in the ring and then in qx, which is sized to hold the rest.
+    static constexpr int TVB = 32 * ROWB;
+    static constexpr int TAIL_LDS = 8 * 2 * TVB;
+    static constexpr int QXA = QX > TAIL_LDS - LDS ? (QX > 1024 ? QX : 1024) : TAIL_LDS - LDS;
+    static_assert(LDS % (2 * TVB) == 0, "a tail wave's buffers lie in one array");
     static_assert(NW == 8 || NW == 16, "eight or sixteen waves");
     static_assert(KW % 32 == 0, "key group slice is whole 32-key blocks");
     static_assert(DMA_PER_STAGE % NW == 0, "DMA split");
@@ -119,17 +138,182 @@ __device__ inline int k_off(int key, int ch) { return key * (2 * D) + 16 * (ch ^
 template <int D>
 __device__ inline int v_off(int key, int ch) { return key * (2 * D) + 16 * (ch ^ ((2 * key) & (D == 128 ? 14 : 6))); }
 
+// Per-stream tail pass, one wave: the G (<= 16) query rows of stream e and
+// kv head g (pair = e * H_kv + g) against the stream's own keys 0 .. n_e - 1
+// (§3.4: a stream's own rows are seen by its own queries only), into slot 0
+// of those rows.  The rows fill one 16-row tile; lanes of rows l16 >= G
+// compute on zero queries and write nothing.  The keys go in 32-key blocks
+// through the wave's own LDS area (buf: K then V, in the items' layouts),
+// filled by DMA (cache rows from a scalar base and 32-bit lane offsets; a
+// block holding a fused append's new row, key n_e - 1, takes per-lane
+// addresses to read that row from k_new / v_new); the arithmetic is the
+// items' (base-2 scores, a reference max raised by more than 8, bf16 P, the
+// normaliser as a product with ones).
+template <int D>
+__device__ inline void tail_pair(const StepArgs& a, uint32_t buf, int pair)
+{
+    constexpr int ROWB = D * 2, CH = D / 8, KSTEPS = D / 32, DT = D / 16, KPI = 1024 / ROWB;
+    constexpr int VSW = D == 128 ? 14 : 6;
+    constexpr int TVB = 32 * ROWB, PIECES = TVB / 1024;
+    const int lane = threadIdx.x & 63, l16 = lane & 15, lg = lane >> 4;
+    const int e = pair / a.H_kv, g = pair - e * a.H_kv;
+    const int n = stream_len(a, e);
+    if (n <= 0) return;  // ended: the finish pass reads no slot of its rows
+    const int an = a.k_new ? appended_row(a, e) : -1;
+    const long kstride = (long)a.H_kv * D;  // elements between key rows of one head
+    const uint16_t* kc = static_cast<const uint16_t*>(a.k_event) + ((long)e * a.cap * a.H_kv + g) * D;
+    const uint16_t* vc = static_cast<const uint16_t*>(a.v_event) + ((long)e * a.cap * a.H_kv + g) * D;
+    const long nrow = ((long)e * a.H_kv + g) * D;
+    const uint16_t* kn = a.k_new ? static_cast<const uint16_t*>(a.k_new) + nrow : kc;
+    const uint16_t* vn = a.k_new ? static_cast<const uint16_t*>(a.v_new) + nrow : vc;
+    const uint32_t kstrideB = (uint32_t)(kstride * 2);
+    const float c = a.qscale;
+    typedef __attribute__((address_space(3))) unsigned char lds_uchar_t;
+    const lds_uchar_t* const kbuf = reinterpret_cast<const lds_uchar_t*>((uintptr_t)buf);
+    const lds_uchar_t* const vbuf = kbuf + TVB;
+
+    // Q^T operands: tile row l16 is query head g*G + l16 of stream e
+    const bool row_ok = l16 < a.G;
+    bf16x8_t qf[KSTEPS];
+    {
+        const uint16_t* q = static_cast<const uint16_t*>(a.q) + ((long)e * a.H_q + g * a.G + (row_ok ? l16 : 0)) * D;
+#pragma unroll
+        for (int t = 0; t < KSTEPS; ++t) {
+            const u32x4_t x = *reinterpret_cast<const u32x4_t*>(q + 32 * t + 8 * lg);
+            qf[t] = as_bf16x8(row_ok ? x : u32x4_t{0u, 0u, 0u, 0u});
+        }
+    }
+    // operand reads (the items' offsets): K key l16, chunk 4t + lg; V^T key
+    // 4 lg + l16 / 4 (+16), d = 16 dt + 4 (l16 % 4) .. +3
+    int koff[KSTEPS], voff[DT];
+#pragma unroll
+    for (int t = 0; t < KSTEPS; ++t) koff[t] = l16 * ROWB + 16 * ((4 * t + lg) ^ (l16 % CH));
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+        const int key = 4 * lg + (l16 >> 2);
+        const int ch = 2 * dt + ((l16 & 3) >> 1);
+        voff[dt] = key * ROWB + 16 * (ch ^ ((2 * key) & VSW)) + 8 * (l16 & 1);
+    }
+
+    f32x4_t o[DT], lsum = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    float m_ref = kMinRef;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) o[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    const bf16x8_t ones = as_bf16x8(u32x4_t{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u});
+
+    // Piece i of a block: keys i*KPI + lane/CH, each lane one 16-byte chunk,
+    // permuted as in the items' K and V areas (the K permutation repeats
+    // every CH/KPI pieces, the V one every 2)
+    constexpr int KREP = CH / KPI;
+    uint32_t kcho[KREP], vcho[2];
+#pragma unroll
+    for (int i = 0; i < KREP; ++i) kcho[i] = 16 * ((lane % CH) ^ ((i * KPI + lane / CH) % CH));
+#pragma unroll
+    for (int i = 0; i < 2; ++i) vcho[i] = 16 * ((lane % CH) ^ ((2 * (i * KPI + lane / CH)) & VSW));
+    for (int kb = 0; kb < n; kb += 32) {
+        if (an >= kb && an < kb + 32) {
+#pragma unroll
+            for (int i = 0; i < PIECES; ++i) {
+                const int key = i * KPI + lane / CH;
+                const int kk = min(kb + key, n - 1);
+                dma_16B(reinterpret_cast<const unsigned char*>(kk == an ? kn : kc + kk * kstride) + kcho[i % KREP],
+                        buf + 1024 * i);
+                dma_16B(reinterpret_cast<const unsigned char*>(kk == an ? vn : vc + kk * kstride) + vcho[i % 2],
+                        buf + TVB + 1024 * i);
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < PIECES; ++i) {
+                const uint32_t row = (uint32_t)min(kb + i * KPI + lane / CH, n - 1) * kstrideB;
+                dma_16B_sbase(kc, row + kcho[i % KREP], buf + 1024 * i);
+                dma_16B_sbase(vc, row + vcho[i % 2], buf + TVB + 1024 * i);
+            }
+        }
+        wave_wait_vmcnt<0>();
+
+        f32x4_t s[2];
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt) {
+            s[kt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int t = 0; t < KSTEPS; ++t) {
+                const bf16x8_t kf = as_bf16x8(
+                    *reinterpret_cast<const __attribute__((address_space(3))) u32x4_t*>(kbuf + 16 * kt * ROWB + koff[t]));
+                s[kt] = mfma_16x16x32(kf, qf[t], s[kt]);
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) s[kt][i] = kb + 16 * kt + 4 * lg + i >= n ? kNegInf : s[kt][i];
+        }
+        const float mx = fmaxf(fmaxf(fmaxf(s[0][0], s[0][1]), fmaxf(s[0][2], s[0][3])),
+                               fmaxf(fmaxf(s[1][0], s[1][1]), fmaxf(s[1][2], s[1][3])));
+        if (__any(mx * c > m_ref + 8.f)) {
+            const float mt = max_over_groups(mx) * c;
+            const bool up = mt > m_ref + 8.f;
+            const float alpha = up ? fast_exp2(m_ref - mt) : 1.f;
+            m_ref = up ? mt : m_ref;
+            lsum *= alpha;
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) o[dt] *= alpha;
+        }
+        float p[8];
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) p[4 * kt + i] = fast_exp2(fmaf(s[kt][i], c, -m_ref));
+        const bf16x8_t pf = as_bf16x8(u32x4_t{pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]),
+                                              pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7])});
+        lsum = mfma_16x16x32(ones, pf, lsum);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+            const lds_uchar_t* va = vbuf + voff[dt];
+            const s16x4_t x0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4_t*)va);
+            const s16x4_t x1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (__attribute__((address_space(3))) s16x4_t*)(va + 16 * ROWB));
+            const u32x2_t xa = __builtin_bit_cast(u32x2_t, x0);
+            const u32x2_t xb = __builtin_bit_cast(u32x2_t, x1);
+            o[dt] = mfma_16x16x32(as_bf16x8(u32x4_t{xa.x, xa.y, xb.x, xb.y}), pf, o[dt]);
+        }
+        // this block's LDS reads are done before the next block's DMA refills buf
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    }
+
+    if (!row_ok) return;
+    const float l = lsum[0];
+    const float inv = l > 0.f ? 1.f / l : 0.f;
+    const long slot = ((long)e * a.H_q + g * a.G + l16) * a.max_chunks;  // slot 0 of the row
+    uint16_t* dst = static_cast<uint16_t*>(a.part_o) + slot * D;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+        const f32x4_t v = o[dt];
+        *reinterpret_cast<uint2*>(dst + 16 * dt + 4 * lg) =
+            make_uint2(pack_bf16x2(v[0] * inv, v[1] * inv), pack_bf16x2(v[2] * inv, v[3] * inv));
+    }
+    if (lg == 0) *reinterpret_cast<float2*>(a.part_ml + 2 * slot) = make_float2(m_ref, l);
+}
+
 template <int D, int NT, int WR, int WK, bool PLAN, bool MQ>
 __global__ __launch_bounds__(64 * WR * WK) void split_mfma_kernel(StepArgs a)
 {
     using C = MfmaCfg<D, NT, WR, WK>;
     __shared__ __attribute__((aligned(1024))) unsigned char lds[C::LDS];
+    __shared__ __attribute__((aligned(1024))) unsigned char qx[C::QXA];
     __shared__ int tab_start[kMaxStreamsPerVideo + 1];
     __shared__ int tab_nlen[kMaxStreamsPerVideo];
     __shared__ int s_total;
 
+    if ((int)blockIdx.x < a.tail_blocks) {
+        // per-stream tail pass: waves 0..7, one (stream, kv head) pair each
+        const int w = threadIdx.x >> 6;
+        const int pair = (int)blockIdx.x * 8 + w;
+        if (w < 8 && pair < a.num_events * a.H_kv) {
+            const int off = w * 2 * C::TVB;
+            tail_pair<D>(a, off < C::LDS ? lds_u32(lds + off) : lds_u32(qx + (off - C::LDS)), pair);
+        }
+        return;
+    }
+
     // ---- which item; every branch below is uniform over the work-group ----
-    const int item = item_of_block(a, blockIdx.x);
+    const int item = item_of_block(a, (int)blockIdx.x - a.tail_blocks);
     if (item < 0) return;
     const ItemId id = item_id(a, item);
     const VideoInfo vi = video_info(a, id.v);
@@ -152,7 +336,12 @@ __global__ __launch_bounds__(64 * WR * WK) void split_mfma_kernel(StepArgs a)
     const int u0 = id.c * upc;
     const bool first_item = id.c == 0 && id.g == 0 && id.rg == 0;
     int u1 = u0 + upc;
-    if (u1 > upre || first_item) {  // reaches own units, or reports the chunk count
+    if (a.tail_blocks > 0) {
+        // the tail pass holds the own units: prefix units only, the chunks
+        // after the tail's slot
+        if (first_item && tid == 0) a.video_chunks[id.v] = min(a.slot0 + (upre + upc - 1) / upc, a.max_chunks);
+        u1 = min(u1, upre);
+    } else if (u1 > upre || first_item) {  // reaches own units, or reports the chunk count
         if (w == 0) {
             const int own = build_unit_table(a, vi, tab_start, tab_nlen);
             if (lane == 0) s_total = upre + own;
@@ -231,36 +420,46 @@ __global__ __launch_bounds__(64 * WR * WK) void split_mfma_kernel(StepArgs a)
         }
     };
 
-    // The first three stages go out before the query rows are read, so the
-    // ring fills while those loads are in flight.
+    // rows of this lane: 16*(rw*NT+nt) + l16 within the item, stream-major
+    const int wrow0 = row0 + 16 * rw * NT;                // first video row of this wave
+    const bool row_wave_active = 16 * rw * NT < nrows;
+
+    // The wave's query rows go out first, then the first NSTAGE-1 stages, all
+    // as DMA: one in-order counter then says when the rows and stage 0 have
+    // landed, and the later stages keep streaming while stage 0 is consumed.
+    // Local row r of the wave sits at byte r*ROWB of its staging area with
+    // the K rows' chunk permutation: bytes below SR in ring slot NSTAGE-1
+    // (the part this wave's own DMA of stage NSTAGE-1 refills, after the
+    // rows are read), the rest in qx.  Rows past the item's last are fetched
+    // from its first row and zeroed after the read.
+    unsigned char* const qslot = lds + (C::NSTAGE - 1) * C::STAGE + w * C::SR;
+    unsigned char* const qext = qx + w * C::XR;
+    const bool q_dma = row_wave_active && nstages > 0;
+    if (q_dma) {
+        const uint16_t* __restrict__ q = static_cast<const uint16_t*>(a.q);
+#pragma unroll
+        for (int j = 0; j < C::QB / 1024; ++j) {
+            const int r = j * C::KPI + lane / C::CH;  // local row
+            const int ir = 16 * rw * NT + r;          // row within the item
+            const long qrow = row_qrow(a, vi, id.g, row0 + (ir < nrows ? ir : 0));
+            const int ch = (lane % C::CH) ^ (r % C::CH);
+            unsigned char* dst = j * 1024 < C::SR ? qslot + j * 1024 : qext + (j * 1024 - C::SR);
+            dma_16B(q + qrow * D + 8 * ch, lds_u32(dst));
+        }
+    }
 #pragma unroll
     for (int st = 0; st < C::NSTAGE - 1; ++st)
         if (st < nstages) issue_stage(st);
 
-    // rows of this lane: 16*(rw*NT+nt) + l16 within the item, stream-major
-    const int wrow0 = row0 + 16 * rw * NT;                // first video row of this wave
-    const bool row_wave_active = 16 * rw * NT < nrows;
     int lane_stream[NT];
     int lane_tok[NT];  // query token of the row within its stream (whole branches; 0 otherwise)
-    bf16x8_t qf[NT][C::KSTEPS];  // Q^T operands: q[row][32t + 8lg .. +7]
-    {
-        const uint16_t* __restrict__ q = static_cast<const uint16_t*>(a.q);
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-            const int r = 16 * (rw * NT + nt) + l16;
-            const bool ok = r < nrows;
-            lane_stream[nt] = ok ? (row0 + r) / (a.G * a.qps) : -2;
-            lane_tok[nt] = ok ? ((row0 + r) / a.G) % a.qps : 0;
-            const long base = ok ? (long)row_qrow(a, vi, id.g, row0 + r) * D : 0;
-#pragma unroll
-            for (int t = 0; t < C::KSTEPS; ++t) {
-                u32x4_t x = {0u, 0u, 0u, 0u};
-                if (ok) x = *reinterpret_cast<const u32x4_t*>(q + base + 32 * t + 8 * lg);
-                qf[nt][t] = as_bf16x8(x);
-            }
-        }
+    for (int nt = 0; nt < NT; ++nt) {
+        const int r = 16 * (rw * NT + nt) + l16;
+        const bool ok = r < nrows;
+        lane_stream[nt] = ok ? (row0 + r) / (a.G * a.qps) : -2;
+        lane_tok[nt] = ok ? ((row0 + r) / a.G) % a.qps : 0;
     }
-    wait_vmcnt<0>();
 
     // Whole branches: the range of query tokens and streams among this
     // wave's rows (uniform over the wave).  No row sees an own key above the
@@ -310,6 +509,7 @@ __global__ __launch_bounds__(64 * WR * WK) void split_mfma_kernel(StepArgs a)
     //  K: key 16kt + l16, chunk 4t + lg.
     //  V: key 4lg + l16/4 (+16), d = 16dt + 4(l16 % 4) .. +3 (8 bytes).
     int koff[C::KSTEPS], voff[C::DT];
+    bf16x8_t qf[NT][C::KSTEPS];  // Q^T operands: q[row][32t + 8lg .. +7], read after stage 0 lands
 #pragma unroll
     for (int t = 0; t < C::KSTEPS; ++t) koff[t] = l16 * C::ROWB + 16 * ((4 * t + lg) ^ (l16 % C::CH));
 #pragma unroll
@@ -434,9 +634,27 @@ __global__ __launch_bounds__(64 * WR * WK) void split_mfma_kernel(StepArgs a)
     for (int st = 0; st < nstages; ++st) {
         // after the barrier every wave's pieces of stage st have landed and
         // stage st-1 has been consumed, so its buffer can be refilled
-        if (st + 2 < nstages) stage_barrier<2 * C::DMA_PER_WAVE>();
-        else if (st + 1 < nstages) stage_barrier<C::DMA_PER_WAVE>();
+        static_assert(C::NSTAGE == 3, "one stage in flight past the consumed one");
+        if (st + 1 < nstages) stage_barrier<C::DMA_PER_WAVE>();
         else stage_barrier<0>();
+        if (st == 0) {
+            // the wave's query rows have landed (they precede stage 0 on its
+            // counter): read the Q^T operands before this wave's DMA below
+            // refills their part of the ring
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) {
+                const bool ok = q_dma && 16 * (rw * NT + nt) + l16 < nrows;
+#pragma unroll
+                for (int t = 0; t < C::KSTEPS; ++t) {
+                    const int off = nt * 16 * C::ROWB + koff[t];
+                    const unsigned char* src = off < C::SR ? qslot + off : qext + (off - C::SR);
+                    u32x4_t x = {0u, 0u, 0u, 0u};
+                    if (q_dma) x = *reinterpret_cast<const u32x4_t*>(src);
+                    qf[nt][t] = as_bf16x8(ok ? x : u32x4_t{0u, 0u, 0u, 0u});
+                }
+            }
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        }
         if (st + C::NSTAGE - 1 < nstages) issue_stage(st + C::NSTAGE - 1);
 
         const UnitInfo ui = unit_info(a, vi, upre, tab_start, tab_nlen, id.g, u0 + st);
@@ -522,7 +740,7 @@ __global__ __launch_bounds__(64 * WR * WK) void split_mfma_kernel(StepArgs a)
         const int r = 16 * (rw * NT + nt) + l16;
         if (r < nrows) {
             const long qr = row_qrow(a, vi, id.g, row0 + r);
-            const long slot = qr * a.max_chunks + id.c;
+            const long slot = qr * a.max_chunks + a.slot0 + id.c;
             // o / l in bf16: a convex combination of V rows, so in V's range
             const float inv = l_part[nt] > 0.f ? 1.f / l_part[nt] : 0.f;
             uint16_t* dst = static_cast<uint16_t*>(a.part_o) + slot * D;

@@ -35,6 +35,7 @@ constexpr int kPathValu = 1;
 constexpr int kPathMfma = 2;
 constexpr int kPathMfma32 = 3;  // override only: the decode step's matrix-core path on 32-row tiles
 constexpr int kTargetItems = 256;   // MI355X compute units: one item per CU
+constexpr int kTailPairs = 8;       // (stream, kv head) pairs per tail work-group: one per wave
 constexpr int kUnitKeys = kUnit;    // keys per unit of the virtual key sequence
 
 std::atomic<int> g_path_override{0};
@@ -99,7 +100,9 @@ struct Plan {
     int shape;          // matrix-core work-group shape (1: 64, 2: 128, 3: 256 rows)
     int rg_max;
     int unit_per_chunk;
-    int max_chunks;
+    int max_chunks;     // slots per row: the tail slot (slot0 = 1) and the chunks
+    int tail_blocks;    // work-groups of the per-stream tail pass (0: own units in the items)
+    int slot0;          // slot of chunk 0
     long n_items;
     size_t part_o_bytes;  // normalised partial outputs
     size_t part_ml_bytes; // (max, normaliser) pairs
@@ -205,7 +208,34 @@ Plan make_plan(const pdec_dims* d, int num_videos)
     upc = std::max<long>(upc, 1);
     p.unit_per_chunk = (int)std::min<long>(upc, 1L << 24);
     p.max_chunks = (int)std::max<long>(1, ceil_div(units_max, p.unit_per_chunk));
-    p.n_items = (long)num_videos * d->num_kv_heads * p.max_chunks * p.rg_max;
+    // A decode step on the 16-row-tile matrix-core kernels with G <= 16 and
+    // more than one chunk takes its streams' own keys in a tail pass of its
+    // own (pdec_common.h): kTailPairs (stream, kv head) pairs per work-group,
+    // a multiple of 8 work-groups so that the items keep their XCD rounds,
+    // and the items cut the prefix units alone, aiming at the compute units
+    // the tail pass leaves.  A tail wave walks its stream's cache in 32-key
+    // blocks, one memory round trip each, about as long as an item's stage:
+    // the pass is taken while a full cache (cap keys) needs at most two
+    // blocks more than an item has stages, so that the tail ends with the
+    // items; a long cache (a single stream decoding alone, say) stays spread
+    // over the chunks as units.  A one-chunk step keeps its own units in the
+    // item, which then writes the result without a finish pass.
+    if (path == kPathMfma && qps == 1 && G <= 16 && p.shape <= 3 && p.max_chunks > 1) {
+        const long pairs = (long)d->num_events * d->num_kv_heads;
+        const long tb = 8 * ceil_div(ceil_div(pairs, kTailPairs), 8);
+        const long target = std::max<long>(kTargetItems - tb, kTargetItems / 2);
+        const long upre_max = ceil_div(d->max_prefix_len, kUnitKeys);
+        long upc_pre = ceil_div(ceil_div(tokens, kUnitKeys) * d->num_kv_heads * p.rg_max, target);
+        upc_pre = std::max<long>(upc_pre, ceil_div(std::max<long>(upre_max, 1), kMaxChunks - 1));
+        upc_pre = std::max<long>(upc_pre, 1);
+        if (ceil_div(d->event_cap, 32) <= upc_pre + 2) {
+            p.unit_per_chunk = (int)std::min<long>(upc_pre, 1L << 24);
+            p.max_chunks = (int)(1 + std::max<long>(1, ceil_div(upre_max, p.unit_per_chunk)));
+            p.tail_blocks = (int)std::min<long>(tb, INT32_MAX);
+            p.slot0 = 1;
+        }
+    }
+    p.n_items = (long)num_videos * d->num_kv_heads * (p.max_chunks - p.slot0) * p.rg_max;
     const size_t rows = (size_t)d->num_events * d->num_q_heads * std::max(d->queries_per_stream, 1);
     const size_t elem = d->dtype == PDEC_DTYPE_BF16 ? 2 : 4;
     p.part_o_bytes = (size_t)p.max_chunks * rows * d->head_dim * elem;  // a multiple of 128 bytes
@@ -332,7 +362,7 @@ int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_pr
     // the 32-row-tile kernels read no appended rows: a fused step keeps 16-row tiles
     if (fa && p.shape >= 4) p.shape = p.shape == 5 ? 2 : 3;
     if (workspace_bytes < p.ws_bytes) return PDEC_ERR_WORKSPACE;
-    if (8 * ceil_div(p.n_items, 8) > (long)INT32_MAX) return PDEC_ERR_UNSUPPORTED;
+    if (8 * ceil_div(p.n_items, 8) + p.tail_blocks > (long)INT32_MAX) return PDEC_ERR_UNSUPPORTED;
     if (debug_mode() &&
         (rc = debug_check_lengths(d, num_videos, event_lens, prefix_len, cu_prefix, cu_events,
                                   static_cast<hipStream_t>(stream))) != PDEC_OK)
@@ -373,6 +403,8 @@ int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_pr
     a.plan_T = d->plan_mask ? d->plan_tokens_per_stream : 0;
     a.qps = std::max(d->queries_per_stream, 1);
     a.cross = d->cross_causal;
+    a.tail_blocks = p.tail_blocks;
+    a.slot0 = p.slot0;
     if (fa) {
         a.k_new = fa->k_new;
         a.v_new = fa->v_new;
@@ -381,7 +413,7 @@ int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_pr
     }
 
     hipStream_t s = static_cast<hipStream_t>(stream);
-    const int grid = 8 * a.items_per_xcd;
+    const int grid = a.tail_blocks + 8 * a.items_per_xcd;
     const bool bf16 = d->dtype == PDEC_DTYPE_BF16;
     hipEvent_t ev_start, ev_stop;
     timer_slot_events(&ev_start, &ev_stop);
@@ -606,6 +638,7 @@ int pdec_describe_plan(const pdec_dims* dims, int32_t num_videos, pdec_plan_info
     info->max_chunks = p.max_chunks;
     info->work_items = (int32_t)std::min<long>(p.n_items, INT32_MAX);
     info->merge_pass = (p.path == kPathMfma && p.max_chunks == 1) ? 0 : 1;
+    info->tail_blocks = p.tail_blocks;
     return PDEC_OK;
 }
 

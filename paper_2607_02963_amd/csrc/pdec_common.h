@@ -18,6 +18,14 @@
 // together — and a stream's own rows are fetched once for its G rows.
 // The finish pass merges the slots of each row.
 //
+// A decode step on the matrix-core kernel instead takes the own units out of
+// the sequence when G <= 16: an own unit concerns only the G rows of one
+// stream, so as a unit of the items it keeps a whole work-group at a stage
+// barrier for one or two waves' work.  A per-stream tail pass inside the
+// same launch gives each (stream, kv head) pair one wave that attends its G
+// rows to the stream's own keys (slot 0), and the items walk the prefix
+// units only (chunk c in slot c + 1).
+//
 // Scores are kept in base-2 units: q is pre-multiplied by scale*log2(e), so
 // exp2 replaces exp and lse = ln(2) * (m + log2 l).
 #pragma once
@@ -72,6 +80,15 @@ struct StepArgs {
     const void* v_new;          // [SE, H_kv, D]
     const int32_t* live;        // [SE] or null (every stream live)
     int32_t* lens_out;          // [SE]
+    // Per-stream tail pass (decode steps on the matrix-core kernel, G <= 16):
+    // the first tail_blocks work-groups of the split launch take the
+    // (stream, kv head) pairs, eight per work-group, each the G rows of its
+    // stream against the stream's own keys, into slot 0 of those rows; the
+    // items then hold prefix units only and chunk c fills slot c + 1
+    // (slot0 = 1).  tail_blocks = 0: own units are units of the virtual key
+    // sequence like the prefix's, chunk c in slot c.
+    int tail_blocks;
+    int slot0;
 };
 
 // Launch of the matrix-core split pass (its own translation unit).
@@ -350,6 +367,16 @@ __device__ inline void dma_16B(const void* src, uint32_t lds_base)
                  : "=&s"(saved)
                  : "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(src)
                  : "memory");
+}
+
+// A wave-uniform address as a 64-bit value the compiler keeps in SGPRs
+// (each half through readfirstlane, widened as an unsigned word).
+__device__ inline uint64_t sgpr_base(const void* p)
+{
+    const uint64_t b = reinterpret_cast<uint64_t>(p);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)b);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(b >> 32));
+    return ((uint64_t)hi << 32) | (uint64_t)lo;
 }
 
 // One wave-wide 16-byte-per-lane DMA into LDS from a scalar base address

@@ -54,7 +54,7 @@ class PlanInfo(ctypes.Structure):
 
     _fields_ = [("path", ctypes.c_int32), ("kernel_shape", ctypes.c_int32), ("rows_per_item", ctypes.c_int32),
                 ("row_groups", ctypes.c_int32), ("chunk_keys", ctypes.c_int32), ("max_chunks", ctypes.c_int32),
-                ("work_items", ctypes.c_int32), ("merge_pass", ctypes.c_int32)]
+                ("work_items", ctypes.c_int32), ("merge_pass", ctypes.c_int32), ("tail_blocks", ctypes.c_int32)]
 
 
 class GroundDims(ctypes.Structure):

@@ -60,15 +60,50 @@ def test_self_plan_mask_leaves_the_work_split_alone():
 
 
 def test_workspace_holds_every_partial_slot():
-    """Slots cover the worst case: every prefix unit plus every stream's cache
-    full (129 rows -> 3 units of 64 keys), cut into chunks of chunk_keys."""
+    """Slots cover the worst case.  With the own units as chunk units (the
+    vector kernel): every prefix unit plus every stream's cache full (129 rows
+    -> 3 units of 64 keys), cut into chunks of chunk_keys.  With the per-stream
+    tail pass (a bf16 decode step on the matrix-core kernel): one slot for the
+    tail plus the prefix units cut into chunks."""
+    f32 = _dims(dtype_code=pdec.PDEC_DTYPE_F32)
+    path, chunk = pdec.query_plan(f32)
+    assert path == pdec.PATH_VALU and chunk % 64 == 0 and pdec.describe_plan(f32)["tail_blocks"] == 0
+    slots = -(-(32768 // 64 + 32 * 3) // (chunk // 64))
+    # normalised outputs in the inputs' type, (max, normaliser) in float32, one chunk count
+    assert pdec.workspace_size(f32) == slots * 32 * 28 * (128 * 4 + 2 * 4) + 4
     d = _dims()
     path, chunk = pdec.query_plan(d)
-    assert chunk % 64 == 0
-    units_max = 32768 // 64 + 32 * 3
-    slots = -(-units_max // (chunk // 64))
-    # normalised outputs in bf16, (max, normaliser) in float32, one chunk count
+    assert path == pdec.PATH_MFMA and chunk % 64 == 0 and pdec.describe_plan(d)["tail_blocks"] > 0
+    slots = 1 + -(-(32768 // 64) // (chunk // 64))
     assert pdec.workspace_size(d) == slots * 32 * 28 * (128 * 2 + 2 * 4) + 4
+
+
+def test_tail_pass_plan():
+    """Which steps take the per-stream tail pass, and its size: 8 (stream, kv
+    head) pairs per work-group, a multiple of 8 work-groups; the items then
+    cut the prefix units alone, after the tail's slot."""
+    d = _dims()                                           # 32 streams x 4 kv heads = 128 pairs
+    info = pdec.describe_plan(d)
+    assert info["tail_blocks"] == 16 and info["merge_pass"] == 1
+    units_per_chunk = info["chunk_keys"] // 64
+    assert info["max_chunks"] == 1 + -(-(32768 // 64) // units_per_chunk)
+    assert info["work_items"] == (info["max_chunks"] - 1) * info["row_groups"] * 4
+    # items aim at the compute units the tail leaves: no more than 256 - 16
+    assert info["work_items"] <= 256 - 16
+    assert pdec.describe_plan(_dims(num_events=33))["tail_blocks"] == 24   # 132 pairs -> 17 -> 24
+    # no tail pass: float32 (vector kernel), whole branches, G > 16, the
+    # 32-row-tile kernel, and a step whose units fit one chunk
+    assert pdec.describe_plan(_dims(dtype_code=pdec.PDEC_DTYPE_F32))["tail_blocks"] == 0
+    mq = pdec.make_dims(8, 28, 4, 128, 16, 1024, pdec.PDEC_DTYPE_BF16, queries_per_stream=4)
+    assert pdec.describe_plan(mq)["tail_blocks"] == 0
+    assert pdec.describe_plan(pdec.make_dims(4, 68, 4, 128, 129, 32768, pdec.PDEC_DTYPE_BF16))["tail_blocks"] == 0
+    one = pdec.make_dims(1024, 64, 8, 128, 8, 64, pdec.PDEC_DTYPE_BF16)  # 32 row groups: one chunk
+    assert pdec.describe_plan(one)["max_chunks"] == 1 and pdec.describe_plan(one)["tail_blocks"] == 0
+    pdec.set_path(pdec.PATH_MFMA32)
+    try:
+        assert pdec.describe_plan(d)["tail_blocks"] == 0
+    finally:
+        pdec.set_path(pdec.PATH_AUTO)
 
 
 @pytest.mark.parametrize("E,G,dt,expect", [(32, 7, pdec.PDEC_DTYPE_BF16, pdec.PATH_MFMA),
@@ -216,7 +251,8 @@ def test_describe_plan_matches_query_plan_and_shapes():
         path, chunk = pdec.query_plan(d)
         assert (info["path"], info["chunk_keys"]) == (path, chunk)
         assert (info["kernel_shape"], info["rows_per_item"], info["row_groups"]) == (shape, rows, groups), (E, info)
-        assert info["work_items"] == info["max_chunks"] * info["row_groups"] * 4
+        slots_per_chunk_cut = info["max_chunks"] - (1 if info["tail_blocks"] else 0)
+        assert info["work_items"] == slots_per_chunk_cut * info["row_groups"] * 4
     with pytest.raises(pdec.PdecError):
         pdec.describe_plan(_dims(H_q=27))
     assert pdec.lib().pdec_describe_plan(ctypes.byref(_dims()), 1, None) == pdec.PDEC_ERR_INVALID_ARG

@@ -52,8 +52,10 @@ def test_noalloc_equals_workspace_entry_point_twice(order):
 
 def test_noalloc_refuses_a_step_beyond_its_scratch():
     """A step whose partial states exceed the static buffer is refused before
-    anything is enqueued (the pointers are never used)."""
-    dims = pdec.make_dims(2048, 28, 4, 128, 4096, 1 << 20, pdec.PDEC_DTYPE_BF16)
+    anything is enqueued (the pointers are never used).  2048 streams x 56
+    query heads at a 1M-token prefix: two slots per row (the tail pass's and
+    one chunk's) of 114688 rows, 60 MB."""
+    dims = pdec.make_dims(2048, 56, 4, 128, 4096, 1 << 20, pdec.PDEC_DTYPE_BF16)
     assert pdec.workspace_size(dims) > pdec.NOALLOC_SCRATCH_BYTES
     p = ctypes.c_void_p(4096)
     rc = pdec.lib().pdec_attn_step_noalloc(ctypes.byref(dims), p, p, p, p, p, p, p, p, p, None)
