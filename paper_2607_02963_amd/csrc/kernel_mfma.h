@@ -86,15 +86,19 @@ __device__ inline float max_over_groups(float x)
 constexpr float kMinRef = -1e30f;
 
 
-template <int D, int NT, int WR, int WK>
+template <int D, int NT, int WR, int WK, bool MQ>
 struct MfmaCfg {
     static constexpr int NW = WR * WK;            // waves
     static constexpr int KS = kUnit;              // keys per stage: one unit
     static constexpr int KW = KS / WK;            // keys per key group per stage
-    // ring slots: two stages in flight while the third is consumed (a ring
-    // probe streams the decode layout as fast with two stages in flight as
-    // with three or four)
-    static constexpr int NSTAGE = 3;
+    // Ring slots.  A decode step keeps two stages in flight while the third
+    // is consumed (a ring probe streams the decode layout as fast with two
+    // stages in flight as with three or four) and stages its query rows by
+    // DMA (QDMA); whole branches, whose items run many matrix-bound stages,
+    // keep three in flight and load their query rows directly (measured
+    // faster: the prefill call 649 against 700 us).
+    static constexpr bool QDMA = !MQ;
+    static constexpr int NSTAGE = QDMA ? 3 : 4;
     static constexpr int ROWB = D * 2;            // bytes per key row
     static constexpr int CH = D / 8;              // 16-byte chunks per key row
     static constexpr int STAGE_K = KS * ROWB;     // bytes of K per stage
@@ -116,14 +120,14 @@ struct MfmaCfg {
     // (SR bytes), and the rest in an area of their own (XR bytes per wave).
     static constexpr int QB = NT * 16 * ROWB;
     static constexpr int SR = STAGE / NW;
-    static constexpr int XR = QB - SR;
+    static constexpr int XR = QDMA ? QB - SR : 0;
     static constexpr int QX = NW * XR;
     static_assert(XR >= 0 && SR % 1024 == 0 && XR % 1024 == 0, "query staging");
     // A tail work-group's eight waves each stage a 32-key K and V block
     // (TVB bytes each) in the ring and then in qx, which is sized to hold the rest.
     static constexpr int TVB = 32 * ROWB;
     static constexpr int TAIL_LDS = 8 * 2 * TVB;
-    static constexpr int QXA = QX > TAIL_LDS - LDS ? (QX > 1024 ? QX : 1024) : TAIL_LDS - LDS;
+    static constexpr int QXA = QX > TAIL_LDS - LDS ? (QX > 1024 ? QX : 1024) : (TAIL_LDS - LDS > 1024 ? TAIL_LDS - LDS : 1024);
     static_assert(LDS % (2 * TVB) == 0, "a tail wave's buffers lie in one array");
     static_assert(NW == 8 || NW == 16, "eight or sixteen waves");
     static_assert(KW % 32 == 0, "key group slice is whole 32-key blocks");
@@ -294,22 +298,26 @@ __device__ inline void tail_pair(const StepArgs& a, uint32_t buf, int pair)
 template <int D, int NT, int WR, int WK, bool PLAN, bool MQ>
 __global__ __launch_bounds__(64 * WR * WK) void split_mfma_kernel(StepArgs a)
 {
-    using C = MfmaCfg<D, NT, WR, WK>;
+    using C = MfmaCfg<D, NT, WR, WK, MQ>;
     __shared__ __attribute__((aligned(1024))) unsigned char lds[C::LDS];
     __shared__ __attribute__((aligned(1024))) unsigned char qx[C::QXA];
     __shared__ int tab_start[kMaxStreamsPerVideo + 1];
     __shared__ int tab_nlen[kMaxStreamsPerVideo];
     __shared__ int s_total;
 
-    if ((int)blockIdx.x < a.tail_blocks) {
-        // per-stream tail pass: waves 0..7, one (stream, kv head) pair each
-        const int w = threadIdx.x >> 6;
-        const int pair = (int)blockIdx.x * 8 + w;
-        if (w < 8 && pair < a.num_events * a.H_kv) {
-            const int off = w * 2 * C::TVB;
-            tail_pair<D>(a, off < C::LDS ? lds_u32(lds + off) : lds_u32(qx + (off - C::LDS)), pair);
+    if constexpr (!MQ) {
+        // per-stream tail pass (decode steps only; the kernels of whole
+        // branches carry none of its code): waves 0..7, one (stream, kv
+        // head) pair each
+        if ((int)blockIdx.x < a.tail_blocks) {
+            const int w = threadIdx.x >> 6;
+            const int pair = (int)blockIdx.x * 8 + w;
+            if (w < 8 && pair < a.num_events * a.H_kv) {
+                const int off = w * 2 * C::TVB;
+                tail_pair<D>(a, off < C::LDS ? lds_u32(lds + off) : lds_u32(qx + (off - C::LDS)), pair);
+            }
+            return;
         }
-        return;
     }
 
     // ---- which item; every branch below is uniform over the work-group ----
@@ -434,7 +442,7 @@ __global__ __launch_bounds__(64 * WR * WK) void split_mfma_kernel(StepArgs a)
     // from its first row and zeroed after the read.
     unsigned char* const qslot = lds + (C::NSTAGE - 1) * C::STAGE + w * C::SR;
     unsigned char* const qext = qx + w * C::XR;
-    const bool q_dma = row_wave_active && nstages > 0;
+    const bool q_dma = C::QDMA && row_wave_active && nstages > 0;
     if (q_dma) {
         const uint16_t* __restrict__ q = static_cast<const uint16_t*>(a.q);
 #pragma unroll
@@ -453,13 +461,27 @@ __global__ __launch_bounds__(64 * WR * WK) void split_mfma_kernel(StepArgs a)
 
     int lane_stream[NT];
     int lane_tok[NT];  // query token of the row within its stream (whole branches; 0 otherwise)
+    bf16x8_t qf[NT][C::KSTEPS];  // Q^T operands: q[row][32t + 8lg .. +7]
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
         const int r = 16 * (rw * NT + nt) + l16;
         const bool ok = r < nrows;
         lane_stream[nt] = ok ? (row0 + r) / (a.G * a.qps) : -2;
         lane_tok[nt] = ok ? ((row0 + r) / a.G) % a.qps : 0;
+        if constexpr (!C::QDMA) {
+            // direct loads, awaited with every stage in flight (plain loads
+            // and DMA share one counter and complete out of order)
+            const uint16_t* __restrict__ q = static_cast<const uint16_t*>(a.q);
+            const long base = ok ? (long)row_qrow(a, vi, id.g, row0 + r) * D : 0;
+#pragma unroll
+            for (int t = 0; t < C::KSTEPS; ++t) {
+                u32x4_t x = {0u, 0u, 0u, 0u};
+                if (ok) x = *reinterpret_cast<const u32x4_t*>(q + base + 32 * t + 8 * lg);
+                qf[nt][t] = as_bf16x8(x);
+            }
+        }
     }
+    if constexpr (!C::QDMA) wait_vmcnt<0>();
 
     // Whole branches: the range of query tokens and streams among this
     // wave's rows (uniform over the wave).  No row sees an own key above the
@@ -509,7 +531,6 @@ __global__ __launch_bounds__(64 * WR * WK) void split_mfma_kernel(StepArgs a)
     //  K: key 16kt + l16, chunk 4t + lg.
     //  V: key 4lg + l16/4 (+16), d = 16dt + 4(l16 % 4) .. +3 (8 bytes).
     int koff[C::KSTEPS], voff[C::DT];
-    bf16x8_t qf[NT][C::KSTEPS];  // Q^T operands: q[row][32t + 8lg .. +7], read after stage 0 lands
 #pragma unroll
     for (int t = 0; t < C::KSTEPS; ++t) koff[t] = l16 * C::ROWB + 16 * ((4 * t + lg) ^ (l16 % C::CH));
 #pragma unroll
@@ -634,10 +655,10 @@ __global__ __launch_bounds__(64 * WR * WK) void split_mfma_kernel(StepArgs a)
     for (int st = 0; st < nstages; ++st) {
         // after the barrier every wave's pieces of stage st have landed and
         // stage st-1 has been consumed, so its buffer can be refilled
-        static_assert(C::NSTAGE == 3, "one stage in flight past the consumed one");
-        if (st + 1 < nstages) stage_barrier<C::DMA_PER_WAVE>();
+        if (C::NSTAGE >= 4 && st + 2 < nstages) stage_barrier<2 * C::DMA_PER_WAVE>();
+        else if (st + 1 < nstages) stage_barrier<C::DMA_PER_WAVE>();
         else stage_barrier<0>();
-        if (st == 0) {
+        if (C::QDMA && st == 0) {
             // the wave's query rows have landed (they precede stage 0 on its
             // counter): read the Q^T operands before this wave's DMA below
             // refills their part of the ring

@@ -5,11 +5,11 @@
 //           16-byte loads, eight in flight per thread, the data folded into a
 //           checksum word.  The ceiling of a bare read of these bytes in one
 //           launch.
-//   mode 1  the split pass's own memory path: work items (kv head, chunk of
-//           keys_per_item keys), every 64-key stage of the head's key and value
-//           rows moved by global_load_lds_dwordx4 into a 4-stage LDS ring
-//           (three stages in flight), one work-group barrier per stage, as in
-//           the split kernels, but nothing computed on the staged keys.
+//   mode 1  the decode split pass's own memory path: work items (kv head,
+//           chunk of keys_per_item keys), every 64-key stage of the head's key
+//           and value rows moved by global_load_lds_dwordx4 into a 3-slot LDS
+//           ring (two stages in flight), one work-group barrier per stage, as
+//           in the split kernels, but nothing computed on the staged keys.
 // Nothing is written except the checksum word, and that only when the data
 // hash to a fixed value, so the reads cannot be optimised away.
 #include <hip/hip_runtime.h>
@@ -52,7 +52,7 @@ __global__ __launch_bounds__(512) void read_plain_kernel(const u32x4_t* k, const
 __global__ __launch_bounds__(512) void read_ring_kernel(const uint16_t* k, const uint16_t* v, int L, int H, int keys,
                                                         int32_t* sink)
 {
-    constexpr int NSTAGE = 4, STAGE_K = kUnit * 256, STAGE = 2 * STAGE_K, PIECES = STAGE / 1024, PPW = PIECES / 8;
+    constexpr int NSTAGE = 3, STAGE_K = kUnit * 256, STAGE = 2 * STAGE_K, PIECES = STAGE / 1024, PPW = PIECES / 8;
     __shared__ __attribute__((aligned(1024))) unsigned char lds[NSTAGE * STAGE];
     const int g = blockIdx.x % H, c = blockIdx.x / H;
     const int k0 = c * keys;
@@ -76,8 +76,7 @@ __global__ __launch_bounds__(512) void read_ring_kernel(const uint16_t* k, const
         if (st < nst) issue(st);
     uint32_t acc = 0;
     for (int st = 0; st < nst; ++st) {
-        if (st + 2 < nst) stage_barrier<2 * PPW>();
-        else if (st + 1 < nst) stage_barrier<PPW>();
+        if (st + 1 < nst) stage_barrier<PPW>();  // stage st + 1 may be in flight
         else stage_barrier<0>();
         if (st + NSTAGE - 1 < nst) issue(st + NSTAGE - 1);
         acc ^= *reinterpret_cast<const uint32_t*>(lds + (st % NSTAGE) * STAGE + 4 * threadIdx.x);
