@@ -221,6 +221,53 @@ def run_read_probe(args, torch, pdec):
                       "results": rows}), flush=True)
 
 
+def run_issue_probe(args, torch, pdec, iters: int = 20000, launches: int = 5):
+    """How a SIMD's matrix-core and vector-ALU work share its time
+    (pdec_issue_probe): per wave and iteration 8 independent bf16 matrix
+    instructions (16x16x32) or 32 FMAs over 8 registers, at 1, 2 and 4 waves
+    per SIMD, both kinds in each wave (mode 2) or half the waves each kind
+    (mode 3).  With both kinds on a SIMD, "serial" is the sum of the parts
+    timed alone and "overlap" their maximum; the measured time says which
+    holds.  For mode 3 at w waves the parts are the w/2-wave times of each
+    kind.  Median of `launches` launches timed with HIP events."""
+    stream = torch.cuda.current_stream()
+    sink = torch.zeros(1, dtype=torch.float32, device="cuda")
+
+    def ns_per_iter(mode, wps):
+        pdec.issue_probe(mode, wps, iters, sink, stream)
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(launches)]
+        for a, b in ev:
+            a.record(stream)
+            pdec.issue_probe(mode, wps, iters, sink, stream)
+            b.record(stream)
+        torch.cuda.synchronize()
+        return float(np.median([a.elapsed_time(b) * 1e6 for a, b in ev])) / iters
+
+    rows, alone = [], {}
+    for wps in (1, 2, 4):
+        m, v, both = ns_per_iter(0, wps), ns_per_iter(1, wps), ns_per_iter(2, wps)
+        alone[wps] = (m, v)
+        row = {"waves_per_simd": wps, "matrix_ns": round(m, 2), "vector_ns": round(v, 2),
+               "both_in_each_wave": {"ns": round(both, 2), "serial": round(m + v, 2), "overlap": round(max(m, v), 2)}}
+        msg = (f"bench: issue probe {wps} waves/SIMD: matrix {m:.1f} ns, vector {v:.1f} ns per iteration; both in "
+               f"each wave {both:.1f} (serial {m + v:.1f}, overlap {max(m, v):.1f})")
+        if wps >= 2:
+            split = ns_per_iter(3, wps)
+            mh, vh = alone[wps // 2]
+            row["half_waves_each"] = {"ns": round(split, 2), "serial": round(mh + vh, 2), "overlap": round(max(mh, vh), 2)}
+            msg += f"; half the waves each {split:.1f} (serial {mh + vh:.1f}, overlap {max(mh, vh):.1f})"
+        rows.append(row)
+        _log(msg)
+    top = rows[-1]
+    # per-instruction SIMD time at 4 waves per SIMD (32 matrix / 128 vector instructions per iteration)
+    print(json.dumps({"metric": "SIMD time per iteration with matrix and vector work (ns)", "value": top["half_waves_each"]["ns"],
+                      "unit": "ns/iteration", "n_gpus": 1, "higher_is_better": False, "data": "synthetic", "dtype": "bf16",
+                      "config": {"workload": "issue_probe", "iterations": iters, "work_groups": 256,
+                                 "matrix_block": "8 x v_mfma_f32_16x16x32_bf16", "vector_block": "32 x v_fma_f32"},
+                      "ns_per_matrix_instruction": round(top["matrix_ns"] / 32, 3),
+                      "ns_per_fma": round(top["vector_ns"] / 128, 3), "results": rows}), flush=True)
+
+
 def loop_split_bytes(lp, s: int) -> int:
     """Algorithmic bytes of the split pass at step s of a decode loop: the
     prefix K/V once per kv head, each live stream's s + 1 own K/V rows and
@@ -756,7 +803,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="long_32k",
                     help="long_32k | single_8k | ragged_16 | tiny_f32 | loop_64 | rope_append | grounding | prefill"
-                         " | aggregation | prefix_causal | prefill_backward | read_probe")
+                         " | aggregation | prefix_causal | prefill_backward | read_probe | issue_probe")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--plan-mask", choices=("full", "self"), default="full",
                     help="full: every stream sees all plan tokens (the full design); self: each stream sees only "
@@ -812,6 +859,9 @@ def main():
         return
     if args.workload == "read_probe":
         run_read_probe(args, torch, pdec)
+        return
+    if args.workload == "issue_probe":
+        run_issue_probe(args, torch, pdec)
         return
     if args.workload == "aggregation":
         run_aggregation(args, torch, pdec, wl)

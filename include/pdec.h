@@ -335,15 +335,35 @@ int pdec_check_lengths(const pdec_dims* dims, int32_t num_videos, const int32_t*
  * bfloat16 in device memory (16-byte aligned), once, computing nothing.
  *   mode 0: plain 16-byte loads, each work-group a contiguous slab (the
  *           HBM read ceiling for these bytes in one launch);
- *   mode 1: the split pass's memory path: items of (kv head, keys_per_item
- *           keys, a multiple of 64), every 64-key stage of the head's key and
- *           value rows moved into a 4-stage LDS ring by direct-to-LDS loads
- *           with a work-group barrier per stage.
+ *   mode 1: the decode split pass's memory path: items of (kv head,
+ *           keys_per_item keys, a multiple of 64), every 64-key stage of the
+ *           head's key and value rows moved into a 3-slot LDS ring (two stages
+ *           in flight) by direct-to-LDS loads with a work-group barrier per
+ *           stage.
  * sink: device int32, written only when the data hash to a fixed value (so
  * the reads cannot be optimised away).  Asynchronous on `stream`.  Returns
  * PDEC_ERR_INVALID_ARG for null or misaligned pointers, L or H_kv < 1, a mode
  * other than 0 or 1, or (mode 1) keys_per_item not a positive multiple of 64.
  */
+/*
+ * Measurement aid (why the split kernel's stages take the sum of their
+ * matrix and vector work): 256 work-groups of 64 * 4 * waves_per_simd lanes
+ * (waves_per_simd 1, 2 or 4 waves on each of a compute unit's four SIMDs),
+ * each wave running `iters` iterations of a fixed instruction block:
+ *   mode 0: eight independent v_mfma_f32_16x16x32_bf16;
+ *   mode 1: thirty-two v_fma_f32 over eight independent registers;
+ *   mode 2: both blocks in every wave, one after the other;
+ *   mode 3: half the waves of each SIMD the matrix block, half the vector
+ *           block (waves_per_simd 2 or 4).
+ * Time the launch on `stream` (HIP events): with both kinds of work on a SIMD
+ * the time is the sum of the parts when the two do not overlap, their
+ * maximum when they do.  sink: a device float, written only in a case that
+ * the inputs never reach.  Asynchronous.  Returns PDEC_ERR_INVALID_ARG for a
+ * null or misaligned sink, a mode outside 0..3, iters < 1, waves_per_simd
+ * not 1, 2 or 4, or mode 3 with one wave per SIMD.
+ */
+int pdec_issue_probe(int32_t mode, int32_t waves_per_simd, int32_t iters, float* sink, void* stream);
+
 int pdec_read_probe(const void* k, const void* v, int32_t L, int32_t H_kv, int32_t keys_per_item, int32_t mode,
                     int32_t* sink, void* stream);
 

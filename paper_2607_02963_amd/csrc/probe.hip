@@ -1,4 +1,5 @@
-// Read-ceiling probes (measurement aid, pdec_read_probe): how fast the device
+// Measurement aids.  pdec_issue_probe: how matrix-core and vector-ALU work
+// share a SIMD (below).  Read-ceiling probes (pdec_read_probe): how fast the device
 // streams a K/V cache pair of the decode step's layout ([L, H_kv, 128] bf16
 // each) once, with no arithmetic.  Two access patterns:
 //   mode 0  plain reads: each work-group streams a contiguous slab with
@@ -84,7 +85,67 @@ __global__ __launch_bounds__(512) void read_ring_kernel(const uint16_t* k, const
     if (acc == kMagic) sink[0] = (int32_t)acc;
 }
 
+// Issue probe: how a SIMD's matrix-core and vector-ALU instructions share
+// its time.  Each wave runs `iters` iterations of a fixed block: kind 0 eight
+// independent v_mfma_f32_16x16x32_bf16 (eight accumulators), kind 1 thirty-two
+// v_fma_f32 over eight independent registers.  Written as assembly so that
+// the blocks are exactly these instructions.  Waves w and w + 4 (w + 8, ...)
+// of a work-group share a SIMD; in the split mode the first half of the
+// waves run kind 0 and the second half kind 1, so every SIMD holds both.
+typedef __attribute__((ext_vector_type(4))) float probe_f32x4_t;
+typedef __attribute__((ext_vector_type(4))) int probe_i32x4_t;
+
+template <int MODE>  // 0 matrix only, 1 vector only, 2 both in each wave, 3 split waves
+__global__ __launch_bounds__(1024) void issue_kernel(int iters, float* sink)
+{
+    const int wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    const bool do_m = MODE == 0 || MODE == 2 || (MODE == 3 && wave < nw / 2);
+    const bool do_v = MODE == 1 || MODE == 2 || (MODE == 3 && wave >= nw / 2);
+    const probe_i32x4_t a = {(int)threadIdx.x, 1, 2, 3}, b = {3, 2, 1, (int)blockIdx.x};
+    probe_f32x4_t c0 = {0.f, 0.f, 0.f, 0.f}, c1 = c0, c2 = c0, c3 = c0, c4 = c0, c5 = c0, c6 = c0, c7 = c0;
+    const float f1 = 1.0001f, f2 = 0.9999f;
+    float x0 = threadIdx.x * 1e-3f, x1 = x0 + 1.f, x2 = x0 + 2.f, x3 = x0 + 3.f, x4 = x0 + 4.f, x5 = x0 + 5.f,
+          x6 = x0 + 6.f, x7 = x0 + 7.f;
+#define PDEC_PROBE_MFMA(acc) asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+v"(acc) : "v"(a), "v"(b))
+#define PDEC_PROBE_FMA(x) asm volatile("v_fma_f32 %0, %1, %2, %0" : "+v"(x) : "v"(f1), "v"(f2))
+    for (int it = 0; it < iters; ++it) {
+        if (do_m) {
+            PDEC_PROBE_MFMA(c0); PDEC_PROBE_MFMA(c1); PDEC_PROBE_MFMA(c2); PDEC_PROBE_MFMA(c3);
+            PDEC_PROBE_MFMA(c4); PDEC_PROBE_MFMA(c5); PDEC_PROBE_MFMA(c6); PDEC_PROBE_MFMA(c7);
+        }
+        if (do_v) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                PDEC_PROBE_FMA(x0); PDEC_PROBE_FMA(x1); PDEC_PROBE_FMA(x2); PDEC_PROBE_FMA(x3);
+                PDEC_PROBE_FMA(x4); PDEC_PROBE_FMA(x5); PDEC_PROBE_FMA(x6); PDEC_PROBE_FMA(x7);
+            }
+        }
+    }
+#undef PDEC_PROBE_MFMA
+#undef PDEC_PROBE_FMA
+    const probe_f32x4_t t = c0 + c1 + c2 + c3 + c4 + c5 + c6 + c7;
+    const float r = t.x + t.y + t.z + t.w + x0 + x1 + x2 + x3 + x4 + x5 + x6 + x7;
+    if (r == 1234.5f) sink[0] = r;  // keeps the loops; never true for these inputs in practice
+}
+
 }  // namespace
+
+extern "C" int pdec_issue_probe(int32_t mode, int32_t waves_per_simd, int32_t iters, float* sink, void* stream)
+{
+    if (!sink || (reinterpret_cast<uintptr_t>(sink) & 3) || mode < 0 || mode > 3 || iters < 1)
+        return PDEC_ERR_INVALID_ARG;
+    if (waves_per_simd != 1 && waves_per_simd != 2 && waves_per_simd != 4) return PDEC_ERR_INVALID_ARG;
+    if (mode == 3 && waves_per_simd < 2) return PDEC_ERR_INVALID_ARG;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const dim3 grid(256), block(256 * waves_per_simd);  // one work-group per compute unit
+    switch (mode) {
+    case 0: hipLaunchKernelGGL(issue_kernel<0>, grid, block, 0, s, (int)iters, sink); break;
+    case 1: hipLaunchKernelGGL(issue_kernel<1>, grid, block, 0, s, (int)iters, sink); break;
+    case 2: hipLaunchKernelGGL(issue_kernel<2>, grid, block, 0, s, (int)iters, sink); break;
+    default: hipLaunchKernelGGL(issue_kernel<3>, grid, block, 0, s, (int)iters, sink); break;
+    }
+    return hipGetLastError() == hipSuccess ? PDEC_OK : PDEC_ERR_HIP;
+}
 
 extern "C" int pdec_read_probe(const void* k, const void* v, int32_t L, int32_t H_kv, int32_t keys_per_item,
                                int32_t mode, int32_t* sink, void* stream)

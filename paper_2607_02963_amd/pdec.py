@@ -32,7 +32,8 @@ EXPORTED = ("pdec_strerror", "pdec_workspace_size", "pdec_attn_step", "pdec_attn
             "pdec_kv_append", "pdec_rope_kv_append", "pdec_set_path", "pdec_query_plan",
             "pdec_set_split_timer", "pdec_describe_plan", "pdec_grounding_workspace_size", "pdec_segment_grounding",
             "pdec_aggregation_workspace_size", "pdec_aggregate", "pdec_backward_workspace_size",
-            "pdec_attn_prefill_backward", "pdec_read_probe", "pdec_check_lengths", "pdec_decode_step")
+            "pdec_attn_prefill_backward", "pdec_read_probe", "pdec_issue_probe", "pdec_check_lengths",
+            "pdec_decode_step")
 
 AGGR_MODES = {"uniform": 0, "learned": 1, "attention": 2}
 
@@ -138,6 +139,8 @@ def lib():
         L.pdec_check_lengths.restype = ctypes.c_int
         L.pdec_check_lengths.argtypes = [dp, i32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                          ctypes.c_void_p]
+        L.pdec_issue_probe.restype = ctypes.c_int
+        L.pdec_issue_probe.argtypes = [i32, i32, i32, ctypes.c_void_p, ctypes.c_void_p]
         L.pdec_read_probe.restype = ctypes.c_int
         L.pdec_read_probe.argtypes = [ctypes.c_void_p, ctypes.c_void_p, i32, i32, i32, i32, ctypes.c_void_p,
                                       ctypes.c_void_p]
@@ -631,6 +634,18 @@ def read_probe(k, v, mode: int, keys_per_item: int = 576, sink=None, stream=None
         sink = torch.zeros(1, dtype=torch.int32, device=k.device)
     _check("pdec_read_probe", lib().pdec_read_probe(k.data_ptr(), v.data_ptr(), k.shape[0], k.shape[1],
                                                     keys_per_item, mode, sink.data_ptr(), _stream(stream, k.device)))
+    return sink
+
+
+def issue_probe(mode: int, waves_per_simd: int, iters: int, sink=None, stream=None, device=None):
+    """pdec_issue_probe: 256 work-groups of waves running `iters` blocks of 8
+    matrix instructions (mode 0), 32 FMAs (mode 1), both (mode 2), or half
+    the waves of each SIMD one and half the other (mode 3)."""
+    dev = torch.device("cuda", torch.cuda.current_device()) if device is None else torch.device(device)
+    if sink is None:
+        sink = torch.zeros(1, dtype=torch.float32, device=dev)
+    _check("pdec_issue_probe", lib().pdec_issue_probe(mode, waves_per_simd, iters, sink.data_ptr(),
+                                                      _stream(stream, dev)))
     return sink
 
 

@@ -293,6 +293,19 @@ def test_read_probe_rejects_bad_arguments_before_launch():
     assert L.pdec_read_probe(fake, fake, 64, 4, 100, 1, fake, None) == pdec.PDEC_ERR_INVALID_ARG
 
 
+def test_issue_probe_rejects_bad_arguments_before_launch():
+    """pdec_issue_probe refuses invalid arguments on the host (no GPU needed)."""
+    L = pdec.lib()
+    fake = 1 << 20  # aligned, never dereferenced: every call below is refused before any launch
+    assert L.pdec_issue_probe(0, 4, 10, None, None) == pdec.PDEC_ERR_INVALID_ARG        # no sink
+    assert L.pdec_issue_probe(0, 4, 10, fake + 2, None) == pdec.PDEC_ERR_INVALID_ARG    # misaligned
+    assert L.pdec_issue_probe(4, 4, 10, fake, None) == pdec.PDEC_ERR_INVALID_ARG        # mode
+    assert L.pdec_issue_probe(-1, 4, 10, fake, None) == pdec.PDEC_ERR_INVALID_ARG
+    assert L.pdec_issue_probe(0, 3, 10, fake, None) == pdec.PDEC_ERR_INVALID_ARG        # waves per SIMD
+    assert L.pdec_issue_probe(0, 4, 0, fake, None) == pdec.PDEC_ERR_INVALID_ARG         # iterations
+    assert L.pdec_issue_probe(3, 1, 10, fake, None) == pdec.PDEC_ERR_INVALID_ARG        # split needs two waves
+
+
 def test_decode_step_refuses_before_launch():
     # fake, aligned, never-dereferenced addresses: each call is refused first
     L = pdec.lib()
