@@ -17,7 +17,15 @@
 // group j (lanes j*LPS ..) takes slots j, j + SPI, ... of a batch of SPI*NB
 // slots, and every load of a batch (partial outputs and (m, l) pairs, slot
 // indices clamped to the last slot so no load needs a branch) is issued
-// before any arithmetic, so a row costs one memory round trip.  The batch
+// before any arithmetic.  In a one-video call (EARLY) the first batch goes out
+// before the row's counts (its stream's length, the chunk count) have
+// arrived, clamped to the planned slot count, which the video then fills
+// but for a prefix shorter than the planned bound, so a row of at most one
+// batch costs one memory round trip: slots past the row's count, which may
+// hold anything, enter no arithmetic (selects, not products with a zero
+// weight).  In a ragged batch the slot count is the longest video's, and
+// the rows of shorter videos would fetch many slots they do not have: there
+// the batch waits for the counts.  The batch
 // maximum is formed over the lane groups by lane exchanges, so every lane
 // weighs its slots with the same M; the weighted sums then meet the same way.
 // Rows with more slots than one batch fold batches in with a rescale.
@@ -31,7 +39,7 @@ constexpr int kMaxChunks = 512;  // largest slot count per row the host plans
 
 typedef __attribute__((ext_vector_type(4))) uint32_t fin_u32x4_t;
 
-template <typename T, int D>
+template <typename T, int D, bool EARLY>
 __global__ __launch_bounds__(256) void finish_kernel(StepArgs a)
 {
     using u32x4_t = fin_u32x4_t;
@@ -51,6 +59,24 @@ __global__ __launch_bounds__(256) void finish_kernel(StepArgs a)
     const int j = lane / LPS;
     const int d0 = EPL * (lane % LPS);
     T* __restrict__ out = static_cast<T*>(a.out) + qr * D + d0;
+    const T* __restrict__ po = static_cast<const T*>(a.part_o) + qr * a.max_chunks * D + d0;
+    const float2* __restrict__ pml = reinterpret_cast<const float2*>(a.part_ml) + qr * a.max_chunks;
+    u32x4_t x[NB];
+    float2 ml[NB];
+    auto load_batch = [&](int c0, int last) {
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+            const int c = min(c0 + j + SPI * i, last);
+            x[i] = *reinterpret_cast<const u32x4_t*>(po + (long)c * D);
+            ml[i] = pml[c];
+        }
+    };
+    if constexpr (EARLY) load_batch(0, a.max_chunks - 1);  // before any other load
+    // the row's counts, loaded once, beside the slots
+    const int vch = a.video_chunks[video_of_event(a, e)];
+    const int n0 = a.event_lens[e];
+    const int live = a.live ? a.live[e] : 1;
+    const int n = stream_len_of(a, n0, live);
 
     // Fused append (one query per stream): the wave of the first query head
     // of kv head g copies stream e's appended K and V rows of head g into the
@@ -58,7 +84,7 @@ __global__ __launch_bounds__(256) void finish_kernel(StepArgs a)
     // of head 0 writes the advanced count.  No other work item of the step
     // touches those cache rows or lens_out.
     const int h = (int)(qr % a.H_q);
-    const int app_n = a.k_new && h % a.G == 0 ? appended_row(a, e) : -1;
+    const int app_n = h % a.G == 0 ? appended_row_of(a, n0, live) : -1;
     constexpr int RCH = D * (int)sizeof(T) / 16;  // 16-byte pieces of one row
     u32x4_t app_x = u32x4_t{0u, 0u, 0u, 0u};
     unsigned char* app_dst = nullptr;
@@ -73,30 +99,30 @@ __global__ __launch_bounds__(256) void finish_kernel(StepArgs a)
         unsigned char* cv = static_cast<unsigned char*>(const_cast<void*>(a.v_event));
         app_dst = (is_v ? cv : ck) + (((long)e * a.cap + app_n) * a.H_kv + h / a.G) * D * (long)sizeof(T) + 16 * piece;
     }
-    if (a.k_new && h == 0 && lane == 0) a.lens_out[e] = stream_len(a, e);
+    if (a.k_new && h == 0 && lane == 0) a.lens_out[e] = n;
 
-    if (stream_len(a, e) <= 0) {  // ended stream: uniform over the wave
-        if (j == 0) *reinterpret_cast<u32x4_t*>(out) = u32x4_t{0u, 0u, 0u, 0u};
-        if (a.lse && lane == 0) a.lse[qr] = kNegInf;
-        return;
+    // an ended stream (uniform over the wave) merges no slot
+    const bool ended = n <= 0;
+    if constexpr (!EARLY) {
+        if (ended) {
+            if (j == 0) *reinterpret_cast<u32x4_t*>(out) = u32x4_t{0u, 0u, 0u, 0u};
+            if (a.lse && lane == 0) a.lse[qr] = kNegInf;
+            return;
+        }
     }
-    const int nch = min(a.video_chunks[video_of_event(a, e)], a.max_chunks);
-    const T* __restrict__ po = static_cast<const T*>(a.part_o) + qr * a.max_chunks * D + d0;
-    const float2* __restrict__ pml = reinterpret_cast<const float2*>(a.part_ml) + qr * a.max_chunks;
+    const int nch = ended ? 0 : min(vch, a.max_chunks);
 
     float M = -1e30f;  // finite: the first rescale multiplies zeros by 2^(-huge) = 0
     float lsum = 0.f;
     float acc[EPL];
 #pragma unroll
     for (int k = 0; k < EPL; ++k) acc[k] = 0.f;
-    for (int c0 = 0; c0 < nch; c0 += BATCH) {
-        u32x4_t x[NB];
-        float2 ml[NB];
+    for (int c0 = 0; EARLY ? c0 == 0 || c0 < nch : c0 < nch; c0 += BATCH) {
+        if (c0 > 0 || !EARLY) load_batch(c0, nch - 1);
+        if constexpr (EARLY) {
 #pragma unroll
-        for (int i = 0; i < NB; ++i) {
-            const int c = min(c0 + j + SPI * i, nch - 1);
-            x[i] = *reinterpret_cast<const u32x4_t*>(po + (long)c * D);
-            ml[i] = pml[c];
+            for (int i = 0; i < NB; ++i)
+                if (c0 + j + SPI * i >= nch) x[i] = u32x4_t{0u, 0u, 0u, 0u};
         }
         float mb = M;
 #pragma unroll
@@ -132,7 +158,10 @@ __global__ __launch_bounds__(256) void finish_kernel(StepArgs a)
 #pragma unroll
         for (int k = 0; k < EPL; ++k) acc[k] += __shfl_xor(acc[k], off);
     }
-    if (j == 0) {
+    if (j == 0 && ended) {
+        *reinterpret_cast<u32x4_t*>(out) = u32x4_t{0u, 0u, 0u, 0u};
+        if (a.lse && lane == 0) a.lse[qr] = kNegInf;
+    } else if (j == 0) {
         const float inv = 1.f / lsum;
         if constexpr (sizeof(T) == 2) {
             u32x4_t y;

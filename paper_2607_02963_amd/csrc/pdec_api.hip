@@ -340,6 +340,20 @@ struct FusedAppend {
     int32_t* lens_out;
 };
 
+// One-video calls issue the first batch of a row's slots before its counts
+// (kernel_finish.h); a ragged batch waits for them.
+template <bool EARLY>
+void launch_finish(const StepArgs& a, bool bf16, int D, int grid, hipStream_t s)
+{
+    if (bf16) {
+        if (D == 128) hipLaunchKernelGGL((finish_kernel<uint16_t, 128, EARLY>), dim3(grid), dim3(256), 0, s, a);
+        else hipLaunchKernelGGL((finish_kernel<uint16_t, 64, EARLY>), dim3(grid), dim3(256), 0, s, a);
+    } else {
+        if (D == 128) hipLaunchKernelGGL((finish_kernel<float, 128, EARLY>), dim3(grid), dim3(256), 0, s, a);
+        else hipLaunchKernelGGL((finish_kernel<float, 64, EARLY>), dim3(grid), dim3(256), 0, s, a);
+    }
+}
+
 int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_prefix, const void* v_prefix,
              const int32_t* cu_prefix, const int32_t* prefix_len, const void* k_event, const void* v_event,
              const int32_t* event_lens, const int32_t* cu_events, void* out, float* lse, void* workspace,
@@ -432,14 +446,8 @@ int run_step(const pdec_dims* d, int num_videos, const void* q, const void* k_pr
     // one chunk per row on the matrix-core path: the split pass wrote the result
     if (p.path == kPathMfma && p.max_chunks == 1) return PDEC_OK;
     const int fgrid = (int)ceil_div(rows, 4);  // four rows per work-group
-    const dim3 fblock(256);
-    if (bf16) {
-        if (d->head_dim == 128) hipLaunchKernelGGL((finish_kernel<uint16_t, 128>), dim3(fgrid), fblock, 0, s, a);
-        else hipLaunchKernelGGL((finish_kernel<uint16_t, 64>), dim3(fgrid), fblock, 0, s, a);
-    } else {
-        if (d->head_dim == 128) hipLaunchKernelGGL((finish_kernel<float, 128>), dim3(fgrid), fblock, 0, s, a);
-        else hipLaunchKernelGGL((finish_kernel<float, 64>), dim3(fgrid), fblock, 0, s, a);
-    }
+    if (num_videos == 1) launch_finish<true>(a, bf16, d->head_dim, fgrid, s);
+    else launch_finish<false>(a, bf16, d->head_dim, fgrid, s);
     return launch_status();
 }
 

@@ -165,15 +165,27 @@ __device__ inline ItemId item_id(const StepArgs& a, int item)
 // Cache row that stream e appends at this step (fused append only; §3.4:
 // a live stream extends its own cache, an ended one stops), or -1: no
 // append, a stream that has ended, or a full cache.
+// From the stream's count before the step (n0 = event_lens[e]) and its live
+// flag (live[e], 1 without a live array).
+__device__ inline int appended_row_of(const StepArgs& a, int n0, int live)
+{
+    return a.k_new && live != 0 && n0 >= 0 && n0 < a.cap ? n0 : -1;
+}
+
 __device__ inline int appended_row(const StepArgs& a, int e)
 {
     if (!a.k_new || (a.live && a.live[e] == 0)) return -1;
-    const int n = a.event_lens[e];
-    return n >= 0 && n < a.cap ? n : -1;
+    return appended_row_of(a, a.event_lens[e], 1);
 }
 
 // Rows of stream e's own cache that the step attends (n_e, the current
 // token included); 0 for a stream that has ended.
+__device__ inline int stream_len_of(const StepArgs& a, int n0, int live)
+{
+    if (!a.k_new) return n0;
+    return live == 0 ? 0 : n0 + (appended_row_of(a, n0, live) >= 0 ? 1 : 0);
+}
+
 __device__ inline int stream_len(const StepArgs& a, int e)
 {
     if (!a.k_new) return a.event_lens[e];
