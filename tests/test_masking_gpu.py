@@ -143,6 +143,33 @@ def test_output_and_workspace_contents_are_ignored(E, path):
     assert _same(o1, o2) and _same(l1, l2)
 
 
+@pytest.mark.parametrize("E", STREAMS, ids=SIDS)
+def test_unfilled_slots_never_enter_the_merge(E, path):
+    """A prefix bound far above the prefix (1100 of 12000 tokens): the step
+    fills a few of the planned slots, and the finish pass's first batch,
+    which in a one-video call goes out before the row's chunk count has
+    arrived, covers all of them.  With the workspace NaN the outputs are
+    bitwise those of a clean workspace, and match the oracle."""
+    s = _step(E)
+    _assert_shape(s, path)
+    d = DevStep(s)
+    bound = 12000
+    dims = pdec.make_dims(s.num_events, s.H_q, s.H_kv, s.D, s.cap, bound, pdec.PDEC_DTYPE_BF16)
+    plan = pdec.describe_plan(dims)
+    if plan["merge_pass"]:
+        assert plan["max_chunks"] >= 2, plan  # at least one slot the step leaves unfilled
+    size = pdec.workspace_size(dims)
+    clean = torch.zeros((size // 4,), dtype=torch.float32, device="cuda")
+    nan = torch.full((size // 4,), float("nan"), dtype=torch.float32, device="cuda")
+    run = lambda ws: pdec.attn_step(d.q, d.k_prefix, d.v_prefix, d.k_event, d.v_event, d.event_lens,
+                                    d.prefix_lens, max_prefix_len=bound, workspace=ws)
+    o1, l1 = run(clean)
+    o2, l2 = run(nan)
+    torch.cuda.synchronize()
+    assert _same(o1, o2) and _same(l1, l2)
+    check("bf16", host(o2), host(l2), *oracle_ref(s))
+
+
 @pytest.mark.parametrize("counts", [(4, 3, 5), (16, 9, 24)], ids=["small", "rows168"])
 def test_other_videos_never_read(counts, path):
     """A ragged batch: the middle video's prefix, caches and queries are NaN
